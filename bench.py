@@ -1,0 +1,369 @@
+#!/usr/bin/env python3
+"""Benchmark of the paged-KV attention hot path on one MI355X.
+
+Headline (the `value`): Qwen3-8B-shaped batched decode, one attention layer -- 32 q-heads,
+8 kv-heads, d=128, bf16, 16-token pages, 64 sequences with cached contexts uniform in
+[2048, 16384], random page placement.  One step = append each sequence's new token K/V into its
+page (kv_append) + decode attention (device planner, split-context attention kernel, split
+merge).  value = decode tokens/s for the layer = 64 / step time.
+
+The same line carries:
+  roofline      HBM roofline of the dominant kernel (the attention kernel), timed with HIP
+                events around each launch inside the timed region;
+  cpu_baseline  the CPU oracle (numpy float64) timed on this host on a bounded sample;
+  secondary     prefill-append TFLOP/s (Qwen3-8B shape), Qwen3-30B-A3B-shaped decode at batch
+                256/128/32, the colocated mixed batch, and kv_append GB/s.
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-secondary] [--no-cpu]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBPS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0       # MI355X dense bf16 MFMA
+METRIC = "paged-attn decode tok/s + HBM TB/s; prefill-append TFLOP/s (Qwen3-8B shape)"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--no-secondary", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--only", default="", help="comma list of secondary workloads to run")
+    ap.add_argument("--cpu-seconds", type=float, default=12.0)
+    return ap.parse_args()
+
+
+# ------------------------------------------------------------------------------------------------
+# algorithmic work (counted from the actual draws)
+# ------------------------------------------------------------------------------------------------
+
+def attn_bytes(case, include_lse=False):
+    """K/V rows attended (read once per sequence and kv-head), Q in, O out, block-table entries."""
+    import numpy as np
+    d, hkv, hq = case.head_dim, case.num_kv_heads, case.num_q_heads
+    keys = case.kv_lens.astype(np.int64)
+    kv = int(keys.sum()) * hkv * d * 2 * 2
+    qo = case.total_q * hq * d * 2 * 2
+    bt = int(((keys + 15) // 16).sum()) * 4
+    lse = case.total_q * hq * 4 if include_lse else 0
+    return kv + qo + bt + lse
+
+
+def attn_flops(case):
+    """4*d per valid (query head, key) pair: 2d for q.k and 2d for p.v."""
+    import numpy as np
+    L = case.ctx_lens.astype(np.int64)
+    n = case.q_lens.astype(np.int64)
+    pairs = int((n * L + n * (n + 1) // 2).sum())
+    return 4 * case.head_dim * case.num_q_heads * pairs
+
+
+def append_bytes(case):
+    return 2 * case.total_q * case.num_kv_heads * case.head_dim * 2 * 2   # K and V, read + write
+
+
+# ------------------------------------------------------------------------------------------------
+# timing
+# ------------------------------------------------------------------------------------------------
+
+class EventPairs:
+    """Raw hipEvent_t pairs handed to the library's timing hook, one pair per timed call."""
+
+    def __init__(self, torch, n):
+        self.torch = torch
+        self.ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+        s = torch.cuda.current_stream()
+        for a, b in self.ev:       # materialise the underlying HIP events
+            a.record(s); b.record(s)
+        torch.cuda.synchronize()
+
+    def handles(self, i):
+        a, b = self.ev[i]
+        return a.cuda_event, b.cuda_event
+
+    def mean_ms(self, n):
+        return sum(a.elapsed_time(b) for a, b in self.ev[:n]) / n
+
+
+def run_timed(torch, pa, step, steps, warmup):
+    """Run `warmup` untimed steps, then `steps` timed steps bracketed by synchronize.  `step(hook)`
+    performs one step and calls hook() right before the library call whose kernel is timed."""
+    pairs = EventPairs(torch, steps)
+    for _ in range(warmup):
+        step(lambda: None)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(steps):
+        h = pairs.handles(i)
+        step(lambda h=h: pa.binding.set_kernel_events(*h))
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    pa.binding.set_kernel_events(None, None)
+    return (t1 - t0) * 1e3 / steps, pairs.mean_ms(steps)
+
+
+# ------------------------------------------------------------------------------------------------
+# workloads
+# ------------------------------------------------------------------------------------------------
+
+def lengths_dev(torch, case):
+    import numpy as np
+    ctx = torch.from_numpy(case.ctx_lens.astype(np.int32)).cuda()
+    cu = torch.from_numpy(case.cu_q_lens.astype(np.int32)).cuda()
+    return ctx, cu
+
+
+def make_step(torch, pa, case, mode):
+    """Closure performing kv_append + attention for `case` through the C ABI with pre-built
+    argument structs (lengths unchanged across steps, so the append rewrites the same slots with
+    the same bytes and every step does identical work)."""
+    import ctypes
+    from paper_2609_35158_amd import binding as bd
+    lib = pa.load()
+    ctx, cu = lengths_dev(torch, case)
+    max_q, max_kv = int(case.q_lens.max()), int(case.kv_lens.max())
+    out = torch.empty_like(case.q)
+    cu_attn = None if mode == "decode" else cu
+    cu_append = None if mode == "decode" else cu
+    shape = bd.make_shape(case.num_q_heads, case.k_pool)
+    desc_attn = bd.make_desc(case.block_table, ctx, cu_attn, case.total_q, max_q, max_kv)
+    desc_app = bd.make_desc(case.block_table, ctx, cu_append, case.total_q, max_q, max_kv)
+    nbytes = lib.pearl_attn_workspace_bytes(ctypes.byref(shape), ctypes.byref(desc_attn))
+    assert nbytes > 0, bd.last_error()
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    fn = {"decode": lib.pearl_attn_decode, "prefill": lib.pearl_attn_prefill_append,
+          "mixed": lib.pearl_attn_mixed}[mode]
+    sp, dp_a, dp_p = ctypes.byref(shape), ctypes.byref(desc_attn), ctypes.byref(desc_app)
+    ptrs = (case.q.data_ptr(), case.k_pool.data_ptr(), case.v_pool.data_ptr())
+    app = (case.k_new.data_ptr(), case.v_new.data_ptr(), case.k_pool.data_ptr(), case.v_pool.data_ptr())
+    stream = torch.cuda.current_stream().cuda_stream
+    scale = ctypes.c_float(case.scale)
+
+    def step(hook, attention=True, append=True):
+        if append:
+            st = lib.pearl_kv_append(sp, dp_p, *app, stream)
+            if st:
+                raise bd.PearlError(st, "pearl_kv_append", bd.last_error())
+        if attention:
+            hook()
+            st = fn(sp, dp_a, *ptrs, scale, out.data_ptr(), None, ws.data_ptr(), nbytes, stream)
+            lib.pearl_set_kernel_events(None, None)
+            if st:
+                raise bd.PearlError(st, mode, bd.last_error())
+    return step, out
+
+
+def time_append(torch, pa, step, steps):
+    def one(hook):
+        hook()
+        step(lambda: None, attention=False)
+        pa.load().pearl_set_kernel_events(None, None)
+    return run_timed(torch, pa, one, steps, 1)
+
+
+# ------------------------------------------------------------------------------------------------
+# CPU oracle baseline on a bounded sample
+# ------------------------------------------------------------------------------------------------
+
+def compact_pool(torch, case, seqs):
+    import numpy as np
+    bt = case.block_table.cpu().numpy()
+    npages = (case.kv_lens + 15) // 16
+    uniq = np.unique(np.concatenate([bt[b, :npages[b]] for b in seqs]))
+    remap = {int(p): i for i, p in enumerate(uniq)}
+    idx = torch.from_numpy(uniq.astype(np.int64)).cuda()
+    as_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    kp = as_bits(case.k_pool.index_select(0, idx))
+    vp = as_bits(case.v_pool.index_select(0, idx))
+    sub_bt = np.zeros((len(seqs), int(npages[list(seqs)].max())), np.int32)
+    for i, b in enumerate(seqs):
+        sub_bt[i, :npages[b]] = [remap[int(p)] for p in bt[b, :npages[b]]]
+    return kp, vp, sub_bt
+
+
+def cpu_baseline(torch, case, out, budget_s):
+    """Time the oracle (single BLAS thread) decoding whole sequences of the same workload until
+    `budget_s` seconds have passed; also report the parity of the GPU output on those sequences."""
+    import numpy as np
+    from threadpoolctl import threadpool_limits
+    import oracle
+    as_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+    q_bits = as_bits(case.q)
+    out_bits = as_bits(out)
+    done, t_total = 0, 0.0
+    errs = []
+    rng = np.random.default_rng(123)
+    order = rng.permutation(case.batch)
+    with threadpool_limits(limits=1):
+        for b in order:
+            kp, vp, sbt = compact_pool(torch, case, [int(b)])
+            t0 = time.perf_counter()
+            o, _ = oracle.attention(q_bits[b:b + 1], kp, vp, sbt, case.ctx_lens[b:b + 1], None, case.scale)
+            t_total += time.perf_counter() - t0
+            done += 1
+            errs.append(oracle.compare(out_bits[b:b + 1], o))
+            if t_total >= budget_s:
+                break
+    keys = int(case.kv_lens[order[:done]].sum())
+    return {
+        "value": done / t_total, "unit": "tok/s", "cores": 1, "kind": "oracle",
+        "sample": "%d of %d sequences of the same decode batch (%d keys, all %d q-heads), numpy float64, "
+                  "1 BLAS thread, %.1f s" % (done, case.batch, keys, case.num_q_heads, t_total),
+        "cpu": cpu_model(),
+    }, {
+        "sequences": done,
+        "max_abs": max(e["max_abs"] for e in errs), "mean_abs": float(np.mean([e["mean_abs"] for e in errs])),
+    }
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip() + " (%d logical CPUs visible)" % len(os.sched_getaffinity(0))
+    except Exception:
+        pass
+    return "unknown"
+
+
+# ------------------------------------------------------------------------------------------------
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path (attention shards by "
+              "sequence and kv-head with no exchange; see the sharding notes). Run with --gpus 1.",
+              file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    import paper_2609_35158_amd as pa
+    from paper_2609_35158_amd import workloads
+    torch.cuda.set_device(0)
+    pa.load()
+    gpu_name = torch.cuda.get_device_name(0)
+    log("bench: device %s" % gpu_name)
+
+    # ---- headline: Qwen3-8B decode, B=64 -------------------------------------------------------
+    log("bench: generating qwen3-8b decode (B=64, ctx U[2048,16384])")
+    case = workloads.qwen3_8b_decode("cuda")
+    step, out = make_step(torch, pa, case, "decode")
+    step(lambda: None)             # first append
+    torch.cuda.synchronize()
+    ms_step, ms_kernel = run_timed(torch, pa, step, args.steps, args.warmup)
+    _, ms_app = time_append(torch, pa, step, args.steps)
+    nbytes = attn_bytes(case)
+    flops = attn_flops(case)
+    tok_s = case.batch / (ms_step * 1e-3)
+    achieved = nbytes / (ms_kernel * 1e-3) / 1e9
+    log("bench: decode step %.3f ms, attention kernel %.3f ms (%.0f GB/s), kv_append %.4f ms"
+        % (ms_step, ms_kernel, achieved, ms_app))
+    result = {
+        "metric": METRIC,
+        "value": round(tok_s, 1),
+        "unit": "tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {
+            "workload": "qwen3-8b-decode: one attention layer, 32 q-heads / 8 kv-heads / d=128, bf16, "
+                        "16-token pages, batch 64, cached context uniform [2048,16384] (seed 1), "
+                        "random page placement; step = kv_append + decode",
+            "batch": case.batch, "keys": int(case.kv_lens.sum()), "head_dim": 128,
+            "num_q_heads": 32, "num_kv_heads": 8, "page_size": 16,
+        },
+        "hbm_tbps_step": round(nbytes / (ms_step * 1e-3) / 1e12, 4),
+        "roofline": {
+            "kernel": "attn_kernel<128> (decode split items)",
+            "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBPS, 4), "traffic": None,
+            "algorithmic_bytes": nbytes, "kernel_ms": round(ms_kernel, 5),
+            "tflops": round(flops / (ms_kernel * 1e-3) / 1e12, 2),
+        },
+        "kv_append": {"kernel_ms": round(ms_app, 5), "bytes": append_bytes(case),
+                      "GBps": round(append_bytes(case) / (ms_app * 1e-3) / 1e9, 1)},
+        "device": gpu_name,
+    }
+    if not args.no_cpu:
+        log("bench: CPU oracle baseline (%.0f s budget)" % args.cpu_seconds)
+        cb, parity = cpu_baseline(torch, case, out, args.cpu_seconds)
+        result["cpu_baseline"] = cb
+        result["parity_sample"] = parity
+        log("bench: cpu %.2f tok/s; parity on %d sequences max_abs %.2e mean_abs %.2e"
+            % (cb["value"], parity["sequences"], parity["max_abs"], parity["mean_abs"]))
+    del case, step, out
+    torch.cuda.empty_cache()
+
+    # ---- secondary workloads ------------------------------------------------------------------
+    if not args.no_secondary:
+        sec = []
+        only = set(x for x in args.only.split(",") if x)
+        specs = [
+            ("qwen3-8b-prefill-append", "prefill", lambda: workloads.qwen3_8b_prefill_append("cuda"), "mfma"),
+            ("qwen3-30b-a3b-decode-b256", "decode", lambda: workloads.qwen3_30b_decode("cuda", batch=256), "hbm"),
+            ("qwen3-30b-a3b-decode-b128", "decode", lambda: workloads.qwen3_30b_decode("cuda", batch=128), "hbm"),
+            ("qwen3-30b-a3b-decode-b32", "decode", lambda: workloads.qwen3_30b_decode("cuda", batch=32), "hbm"),
+            ("mixed-colocated", "mixed", lambda: workloads.mixed_colocated("cuda"), "both"),
+        ]
+        for name, mode, gen, bound in specs:
+            if only and name not in only:
+                continue
+            log("bench: secondary %s" % name)
+            c = gen()
+            st, o = make_step(torch, pa, c, mode)
+            st(lambda: None)
+            torch.cuda.synchronize()
+            ms_s, ms_k = run_timed(torch, pa, st, args.steps, args.warmup)
+            _, ms_a = time_append(torch, pa, st, args.steps)
+            b_ = attn_bytes(c)
+            f_ = attn_flops(c)
+            entry = {"workload": name, "mode": mode, "ms_per_step": round(ms_s, 5), "kernel_ms": round(ms_k, 5),
+                     "batch": c.batch, "new_tokens": c.total_q, "keys": int(c.kv_lens.sum()),
+                     "algorithmic_bytes": b_, "flops": f_,
+                     "GBps": round(b_ / (ms_k * 1e-3) / 1e9, 1),
+                     "TFLOPs": round(f_ / (ms_k * 1e-3) / 1e12, 2),
+                     "kv_append_ms": round(ms_a, 5),
+                     "kv_append_GBps": round(append_bytes(c) / (ms_a * 1e-3) / 1e9, 1)}
+            if mode == "decode":
+                entry["tok_s"] = round(c.batch / (ms_s * 1e-3), 1)
+                entry["frac_hbm"] = round(entry["GBps"] / HBM_PEAK_GBPS, 4)
+            elif mode == "prefill":
+                entry["frac_mfma"] = round(entry["TFLOPs"] / BF16_PEAK_TFLOPS, 4)
+            else:
+                t_hbm = b_ / (HBM_PEAK_GBPS * 1e9) * 1e3
+                t_mfma = f_ / (BF16_PEAK_TFLOPS * 1e12) * 1e3
+                entry["roofline_ms_overlapped"] = round(max(t_hbm, t_mfma), 4)
+                entry["roofline_ms_serial"] = round(t_hbm + t_mfma, 4)
+                entry["frac_of_overlapped_bound"] = round(max(t_hbm, t_mfma) / ms_k, 4)
+            log("bench:   %s" % json.dumps(entry))
+            sec.append(entry)
+            del c, st, o
+            torch.cuda.empty_cache()
+        result["secondary"] = sec
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,311 @@
+// C-ABI host layer: argument validation, workspace layout, launch sequencing and error mapping for
+// the gfx950 paged-KV attention kernels.  The interface and its contract are documented in
+// include/pearl_attn.h.
+
+#include "../../include/pearl_attn.h"
+#include "pearl_internal.h"
+
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+
+namespace pearl {
+namespace {
+
+thread_local char g_err[512] = "";
+thread_local hipEvent_t g_ev_before = nullptr;
+thread_local hipEvent_t g_ev_after = nullptr;
+
+hipError_t record_before(hipStream_t s) { return g_ev_before ? hipEventRecord(g_ev_before, s) : hipSuccess; }
+hipError_t record_after(hipStream_t s) { return g_ev_after ? hipEventRecord(g_ev_after, s) : hipSuccess; }
+
+void set_err(const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+}
+
+pearl_status fail(pearl_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool debug_mode() {
+  const char* e = std::getenv("PEARL_DEBUG");
+  return e && e[0] && e[0] != '0';
+}
+
+// Shape checks shared by every entry point.
+pearl_status check_shape(const pearl_kv_shape* s) {
+  if (!s) return fail(PEARL_ERR_INVALID_ARG, "shape is NULL");
+  if (s->num_q_heads <= 0 || s->num_kv_heads <= 0)
+    return fail(PEARL_ERR_INVALID_ARG, "num_q_heads (%d) and num_kv_heads (%d) must be > 0", s->num_q_heads, s->num_kv_heads);
+  if (s->num_q_heads % s->num_kv_heads != 0)
+    return fail(PEARL_ERR_INVALID_ARG, "num_q_heads (%d) is not a multiple of num_kv_heads (%d)", s->num_q_heads, s->num_kv_heads);
+  const int G = s->num_q_heads / s->num_kv_heads;
+  if (G != 1 && G != 2 && G != 4 && G != 8)
+    return fail(PEARL_ERR_UNSUPPORTED, "query heads per kv-head G=%d not in {1,2,4,8}", G);
+  if (s->head_dim != 64 && s->head_dim != 128)
+    return fail(PEARL_ERR_UNSUPPORTED, "head_dim %d not in {64,128}", s->head_dim);
+  if (s->page_size != kPage) return fail(PEARL_ERR_UNSUPPORTED, "page_size %d != 16", s->page_size);
+  if (s->num_pages <= 0) return fail(PEARL_ERR_INVALID_ARG, "num_pages (%d) must be > 0", s->num_pages);
+  return PEARL_OK;
+}
+
+pearl_status check_seqs(const pearl_seq_desc* q, bool need_q_lens) {
+  if (!q) return fail(PEARL_ERR_INVALID_ARG, "seqs is NULL");
+  if (q->batch <= 0) return fail(PEARL_ERR_INVALID_ARG, "batch (%d) must be > 0", q->batch);
+  if (!q->block_table) return fail(PEARL_ERR_INVALID_ARG, "block_table is NULL");
+  if (!q->ctx_lens) return fail(PEARL_ERR_INVALID_ARG, "ctx_lens is NULL");
+  if (q->bt_stride <= 0) return fail(PEARL_ERR_INVALID_ARG, "bt_stride (%d) must be > 0", q->bt_stride);
+  if (q->total_q < 0 || q->max_q_len < 0 || q->max_kv_len < 0)
+    return fail(PEARL_ERR_INVALID_ARG, "total_q, max_q_len and max_kv_len must be >= 0");
+  if (need_q_lens && !q->cu_q_lens) return fail(PEARL_ERR_INVALID_ARG, "cu_q_lens is NULL");
+  if (!q->cu_q_lens) {
+    if (q->total_q != q->batch)
+      return fail(PEARL_ERR_INVALID_ARG, "cu_q_lens is NULL (one token per sequence) but total_q (%d) != batch (%d)", q->total_q, q->batch);
+    if (q->max_q_len < 1) return fail(PEARL_ERR_INVALID_ARG, "max_q_len (%d) < 1 with one token per sequence", q->max_q_len);
+  }
+  if (q->max_q_len > q->total_q) return fail(PEARL_ERR_INVALID_ARG, "max_q_len (%d) > total_q (%d)", q->max_q_len, q->total_q);
+  if (q->max_q_len > q->max_kv_len && q->total_q > 0)
+    return fail(PEARL_ERR_INVALID_ARG, "max_q_len (%d) > max_kv_len (%d)", q->max_q_len, q->max_kv_len);
+  if ((int64_t)q->bt_stride * kPage < q->max_kv_len)
+    return fail(PEARL_ERR_INVALID_ARG, "bt_stride (%d) pages cannot hold max_kv_len (%d) tokens", q->bt_stride, q->max_kv_len);
+  if ((int64_t)q->batch * q->bt_stride > INT32_MAX)
+    return fail(PEARL_ERR_INVALID_ARG, "block table too large");
+  return PEARL_OK;
+}
+
+struct Plan {
+  PlanParams p;
+  WsLayout lay;
+};
+
+Plan make_plan(const pearl_kv_shape* s, const pearl_seq_desc* q, int mode) {
+  Plan pl;
+  const int G = s->num_q_heads / s->num_kv_heads;
+  const int pps = choose_pages_per_split(q->batch, s->num_kv_heads, q->max_kv_len, kPlanComputeUnits);
+  pl.lay = workspace_layout(q->batch, q->total_q, q->max_kv_len, s->num_q_heads, s->num_kv_heads, s->head_dim, G, pps);
+  PlanParams& p = pl.p;
+  p.mode = mode;
+  p.batch = q->batch;
+  p.total_q = q->total_q;
+  p.max_q_len = q->max_q_len;
+  p.max_kv_len = q->max_kv_len;
+  p.bt_stride = q->bt_stride;
+  p.num_kv_heads = s->num_kv_heads;
+  p.group = G;
+  p.tokens_per_tile = kRowsPerTile / G;
+  p.pages_per_split = pps;
+  p.max_pre = pl.lay.max_pre;
+  p.max_dec = pl.lay.max_dec;
+  return pl;
+}
+
+pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_desc* q, const void* qp,
+                           const void* k_pool, const void* v_pool, float scale, void* out, float* lse,
+                           void* ws, size_t ws_bytes, void* stream) {
+  g_err[0] = 0;
+  pearl_status st = check_shape(s);
+  if (st != PEARL_OK) return st;
+  st = check_seqs(q, mode == kModeMixed);
+  if (st != PEARL_OK) return st;
+  if (mode == kModeDecode && q->cu_q_lens)
+    return fail(PEARL_ERR_INVALID_ARG, "pearl_attn_decode requires cu_q_lens == NULL (one token per sequence)");
+  if (!qp || !k_pool || !v_pool || !out) return fail(PEARL_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be non-NULL");
+  if (!ws) return fail(PEARL_ERR_WORKSPACE, "workspace is NULL");
+  if (!aligned16(qp) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
+    return fail(PEARL_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
+  if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(PEARL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (lse && (reinterpret_cast<uintptr_t>(lse) & 3) != 0) return fail(PEARL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
+  if (!(scale > 0.f) || !std::isfinite(scale)) return fail(PEARL_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
+  const int64_t total_rows = (int64_t)q->total_q * s->num_q_heads * s->head_dim;
+  if (total_rows > INT32_MAX * int64_t(8)) return fail(PEARL_ERR_UNSUPPORTED, "q/out too large");
+  Plan pl = make_plan(s, q, mode);
+  if (ws_bytes < pl.lay.total)
+    return fail(PEARL_ERR_WORKSPACE, "workspace_bytes %zu < required %zu", ws_bytes, pl.lay.total);
+  hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+  char* w = static_cast<char*>(ws);
+  hipError_t e = launch_plan(pl.p, q->ctx_lens, q->cu_q_lens, ws, pl.lay, hs);
+  if (e != hipSuccess) return fail(PEARL_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+  AttnArgs a;
+  a.q = static_cast<const uint16_t*>(qp);
+  a.k_pool = static_cast<const uint16_t*>(k_pool);
+  a.v_pool = static_cast<const uint16_t*>(v_pool);
+  a.block_table = q->block_table;
+  a.out = static_cast<uint16_t*>(out);
+  a.lse = lse;
+  a.ws_hdr = reinterpret_cast<int32_t*>(w + pl.lay.hdr);
+  a.seqinfo = reinterpret_cast<const SeqInfo*>(w + pl.lay.seqinfo);
+  a.split_base = reinterpret_cast<const int32_t*>(w + pl.lay.split_base);
+  a.entries = reinterpret_cast<const int2*>(w + pl.lay.entries);
+  a.part_o = reinterpret_cast<float*>(w + pl.lay.part_o);
+  a.part_ml = reinterpret_cast<float*>(w + pl.lay.part_ml);
+  a.bt_stride = q->bt_stride;
+  a.num_pages = s->num_pages;
+  a.num_q_heads = s->num_q_heads;
+  a.num_kv_heads = s->num_kv_heads;
+  a.group = pl.p.group;
+  a.tokens_per_tile = pl.p.tokens_per_tile;
+  a.pages_per_split = pl.p.pages_per_split;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const int64_t max_items = (pl.lay.max_pre + pl.lay.max_dec) * s->num_kv_heads;
+  e = record_before(hs);
+  if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
+  e = launch_attention(a, s->head_dim, max_items, (int)pl.lay.max_pre, hs);
+  if (e != hipSuccess) return fail(PEARL_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
+  e = record_after(hs);
+  if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
+  if (mode != kModePrefill && pl.lay.max_dec > 0) {
+    e = launch_merge(a, s->head_dim, q->batch, hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "merge launch: %s", hipGetErrorString(e));
+  }
+  if (debug_mode()) {
+    e = hipStreamSynchronize(hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "PEARL_DEBUG sync: %s", hipGetErrorString(e));
+    int32_t flag = 0;
+    e = hipMemcpy(&flag, w + pl.lay.hdr + 4 * kHdrError, sizeof(flag), hipMemcpyDeviceToHost);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "PEARL_DEBUG readback: %s", hipGetErrorString(e));
+    if (flag == 1) return fail(PEARL_ERR_INVALID_ARG, "device lengths violate the host bounds (total_q/max_q_len/max_kv_len/bt_stride) or decode q_len != 1; nothing was computed");
+    if (flag != 0) return fail(PEARL_ERR_INVALID_ARG, "work list exceeded its capacity; nothing was computed");
+  }
+  return PEARL_OK;
+}
+
+}  // namespace
+
+int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu) {
+  // Aim for about 16 decode items per compute unit when every sequence is as long as the bound;
+  // a split never holds fewer than 16 pages (one page pair for each of the 8 waves), and its size
+  // is a multiple of 16 pages.
+  const int64_t max_pages = std::max<int64_t>(1, cdiv(std::max(max_kv_len, 1), kPage));
+  const int64_t target = std::max<int64_t>(1, (int64_t)num_cu * 16);
+  int64_t pps = cdiv((int64_t)batch * num_kv_heads * max_pages, target);
+  pps = std::max<int64_t>(pps, kMinPagesPerSplit);
+  pps = cdiv(pps, 16) * 16;
+  if (pps > (int64_t)1 << 20) pps = (int64_t)1 << 20;
+  return (int)pps;
+}
+
+WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_heads, int num_kv_heads,
+                          int head_dim, int group, int pages_per_split) {
+  WsLayout l;
+  const int T = kRowsPerTile / group;
+  // prefill entries: sum_b ceil(n_b / T) <= total_q / T + batch, and <= total_q
+  l.max_pre = std::min<int64_t>(total_q, total_q / T + batch);
+  // decode entries: every sequence holds at most ceil(max_kv_len / 16) pages
+  const int64_t max_pages = cdiv(std::max(max_kv_len, 1), kPage);
+  l.max_dec = (int64_t)batch * cdiv(max_pages, pages_per_split);
+  size_t off = 0;
+  l.hdr = off; off = align256(off + sizeof(int32_t) * kHdrWords);
+  l.seqinfo = off; off = align256(off + sizeof(SeqInfo) * (size_t)batch);
+  l.split_base = off; off = align256(off + sizeof(int32_t) * (size_t)batch);
+  l.entries = off; off = align256(off + sizeof(int2) * (size_t)(l.max_pre + l.max_dec));
+  l.part_o = off; off = align256(off + sizeof(float) * (size_t)l.max_dec * num_q_heads * head_dim);
+  l.part_ml = off; off = align256(off + sizeof(float) * 2 * (size_t)l.max_dec * num_q_heads);
+  l.total = off;
+  (void)num_kv_heads;
+  return l;
+}
+
+}  // namespace pearl
+
+using namespace pearl;
+
+extern "C" {
+
+int pearl_abi_version(void) { return PEARL_ABI_VERSION; }
+
+const char* pearl_status_str(pearl_status st) {
+  switch (st) {
+    case PEARL_OK: return "PEARL_OK";
+    case PEARL_ERR_INVALID_ARG: return "PEARL_ERR_INVALID_ARG";
+    case PEARL_ERR_UNSUPPORTED: return "PEARL_ERR_UNSUPPORTED";
+    case PEARL_ERR_WORKSPACE: return "PEARL_ERR_WORKSPACE";
+    case PEARL_ERR_HIP: return "PEARL_ERR_HIP";
+  }
+  return "PEARL_ERR_UNKNOWN";
+}
+
+const char* pearl_last_error(void) { return g_err; }
+
+pearl_status pearl_kv_append(const pearl_kv_shape* shape, const pearl_seq_desc* seqs, const void* k_new,
+                             const void* v_new, void* k_pool, void* v_pool, void* stream) {
+  try {
+    g_err[0] = 0;
+    pearl_status st = check_shape(shape);
+    if (st != PEARL_OK) return st;
+    st = check_seqs(seqs, false);
+    if (st != PEARL_OK) return st;
+    if (seqs->total_q == 0) return PEARL_OK;
+    if (!k_new || !v_new || !k_pool || !v_pool) return fail(PEARL_ERR_INVALID_ARG, "k_new, v_new, k_pool and v_pool must be non-NULL");
+    if (!aligned16(k_new) || !aligned16(v_new) || !aligned16(k_pool) || !aligned16(v_pool))
+      return fail(PEARL_ERR_INVALID_ARG, "k_new, v_new, k_pool and v_pool must be 16-byte aligned");
+    hipError_t e = record_before(reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
+    e = launch_kv_append(static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                                    static_cast<uint16_t*>(k_pool), static_cast<uint16_t*>(v_pool), seqs->block_table,
+                                    seqs->bt_stride, seqs->ctx_lens, seqs->cu_q_lens, seqs->batch, seqs->max_q_len,
+                                    shape->num_kv_heads, shape->head_dim, shape->num_pages, seqs->total_q,
+                                    reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "kv_append launch: %s", hipGetErrorString(e));
+    e = record_after(reinterpret_cast<hipStream_t>(stream));
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
+    return PEARL_OK;
+  } catch (...) {
+    return fail(PEARL_ERR_HIP, "unexpected exception in pearl_kv_append");
+  }
+}
+
+void pearl_set_kernel_events(void* before, void* after) {
+  g_ev_before = reinterpret_cast<hipEvent_t>(before);
+  g_ev_after = reinterpret_cast<hipEvent_t>(after);
+}
+
+size_t pearl_attn_workspace_bytes(const pearl_kv_shape* shape, const pearl_seq_desc* seqs) {
+  try {
+    g_err[0] = 0;
+    if (check_shape(shape) != PEARL_OK) return 0;
+    if (check_seqs(seqs, false) != PEARL_OK) return 0;
+    const int G = shape->num_q_heads / shape->num_kv_heads;
+    const int pps = choose_pages_per_split(seqs->batch, shape->num_kv_heads, seqs->max_kv_len, kPlanComputeUnits);
+    return workspace_layout(seqs->batch, seqs->total_q, seqs->max_kv_len, shape->num_q_heads, shape->num_kv_heads,
+                            shape->head_dim, G, pps).total;
+  } catch (...) {
+    set_err("unexpected exception in pearl_attn_workspace_bytes");
+    return 0;
+  }
+}
+
+#define PEARL_ATTN_ENTRY(NAME, MODE)                                                                       \
+  pearl_status NAME(const pearl_kv_shape* shape, const pearl_seq_desc* seqs, const void* q, const void* k_pool, \
+                    const void* v_pool, float softmax_scale, void* out, float* lse, void* workspace,         \
+                    size_t workspace_bytes, void* stream) {                                                \
+    try {                                                                                                  \
+      return run_attention(MODE, shape, seqs, q, k_pool, v_pool, softmax_scale, out, lse, workspace,      \
+                           workspace_bytes, stream);                                                       \
+    } catch (...) {                                                                                        \
+      return fail(PEARL_ERR_HIP, "unexpected exception in " #NAME);                                         \
+    }                                                                                                      \
+  }
+
+PEARL_ATTN_ENTRY(pearl_attn_prefill_append, kModePrefill)
+PEARL_ATTN_ENTRY(pearl_attn_decode, kModeDecode)
+PEARL_ATTN_ENTRY(pearl_attn_mixed, kModeMixed)
+
+}  // extern "C"

@@ -1,0 +1,706 @@
+// gfx950 (MI355X) kernels for paged-KV GQA attention: kv_append scatter, the device-side work
+// planner, the persistent attention kernel (prefill-append tiles on bf16 MFMA and split-context
+// decode items in one grid), and the split merge.
+//
+// The computation: new tokens of each sequence attend causally within their chunk and fully to
+// the cached context (paper, Background: context growth p_{t+1} = p_t + r_t + o_t; Motivation:
+// prefix caching and chunked prefill batched with decode; section 4.3, Eq. 1: decode cost per
+// sequence is its KV-cache read).  Scores are s_j = scale * q.k_j over keys j <= position; the
+// softmax is evaluated online in base 2 (exp(x) = 2^(x log2 e)), fp32 state, bf16 operands.
+// The row sum l accumulates the fp32 weights (so the LSE is accurate to fp32); the weights enter
+// the P.V product rounded to bf16 (round to nearest even).
+//
+// MFMA lane layouts used below (gfx950, bf16, fp32 accumulate; lane l of a 64-lane wave):
+//   32x32x16: A row l%32, k 8*(l/32)+e;  B col l%32, k 8*(l/32)+e;
+//             D col l%32, row (r%4) + 8*(r/4) + 4*(l/32) for accumulator r = 0..15.
+//   16x16x32: A row l%16, k 8*(l/16)+e;  B col l%16, k 8*(l/16)+e;
+//             D col l%16, row 4*(l/16) + r for r = 0..3.
+// The contraction index k may be any permutation of the reduced dimension as long as A and B
+// use the same one; the P.V products below use that freedom so the probabilities feed the B
+// operand straight from the score accumulators.
+//
+// LDS transpose read (ds_read_b64_tr_b16): inside each 16-lane group, lane j supplies the
+// address of an 8-byte row; lane l receives element l%4 of the rows supplied by lanes l/4,
+// l/4+4, l/4+8, l/4+12.  With lane j addressing V[kbase + j/4][dbase + 4*(j%4)] (V row-major,
+// keys x dims), lane l receives V[kbase + i][dbase + l%16] for i = 0..3: four consecutive keys
+// of one dim, i.e. a k-contiguous MFMA operand of V^T.
+
+#include "pearl_internal.h"
+
+#include <math.h>
+
+namespace pearl {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+
+#define LDS_AS __attribute__((address_space(3)))
+
+constexpr float kLn2 = 0.69314718055994530942f;
+
+__device__ __forceinline__ u32x4 ld16(const uint16_t* p) { return *reinterpret_cast<const u32x4*>(p); }
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+__device__ __forceinline__ bf16x8 zero_bf16x8() { return as_bf16x8(u32x4{0u, 0u, 0u, 0u}); }
+
+__device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+__device__ __forceinline__ float flog2(float x) { return __builtin_amdgcn_logf(x); }
+
+__device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
+
+__device__ __forceinline__ i16x4 lds_read_tr(const char* base, int byte_off) {
+  // generic -> LDS address-space cast (the pointer always points into __shared__ memory)
+  LDS_AS i16x4* p = (LDS_AS i16x4*)((LDS_AS char*)(base) + byte_off);
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16(p);
+}
+
+__device__ __forceinline__ bf16x8 concat_tr(i16x4 a, i16x4 b) {
+  typedef short i16x8 __attribute__((ext_vector_type(8)));
+  i16x8 v = {a[0], a[1], a[2], a[3], b[0], b[1], b[2], b[3]};
+  return __builtin_bit_cast(bf16x8, v);
+}
+
+__device__ __forceinline__ int clamp_page(int p, int num_pages) {
+  return p < 0 ? 0 : (p >= num_pages ? num_pages - 1 : p);
+}
+
+// LDS row strides (bytes) of staged K and V tiles: row = one key, padded against bank conflicts.
+template <int D> struct Lds {
+  static constexpr int kStride = D * 2 + 16;
+  static constexpr int vStride = D * 2 + 32;
+  static constexpr int prefill_bytes = 2 * kKeysPerStage * (kStride + vStride);
+  static constexpr int decode_v_bytes = kWaves * 32 * vStride;
+  static constexpr int merge_bytes = kWaves * 8 * D * 4 + 2 * kWaves * 8 * 4;
+  static constexpr int decode_bytes = decode_v_bytes > merge_bytes ? decode_v_bytes : merge_bytes;
+  static constexpr int bytes = prefill_bytes > decode_bytes ? prefill_bytes : decode_bytes;
+};
+
+// ------------------------------------------------------------------------------------------------
+// kv_append: each thread copies one 16-byte chunk of a (token, kv-head) row of K and of V.
+// ------------------------------------------------------------------------------------------------
+constexpr int kAppendTokensPerBlock = 16;
+
+__global__ __launch_bounds__(256) void kv_append_kernel(
+    const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_pool,
+    u32x4* __restrict__ v_pool, const int32_t* __restrict__ bt, int bt_stride,
+    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ cu, int num_kv_heads,
+    int chunks_per_row, int num_pages, int total_q) {
+  const int b = blockIdx.y;
+  const int t0 = blockIdx.x * kAppendTokensPerBlock;
+  const int q_start = cu ? cu[b] : b;
+  const int q_len = cu ? cu[b + 1] - q_start : 1;
+  const int ctx = ctx_lens[b];
+  const int n_tok = min(kAppendTokensPerBlock, q_len - t0);
+  if (n_tok <= 0 || q_start < 0 || ctx < 0) return;
+  const int per_tok = num_kv_heads * chunks_per_row;
+  const int total = n_tok * per_tok;
+  for (int i = threadIdx.x; i < total; i += blockDim.x) {
+    const int t = t0 + i / per_tok;
+    const int rem = i - (i / per_tok) * per_tok;
+    const int h = rem / chunks_per_row;
+    const int c = rem - h * chunks_per_row;
+    const int pos = ctx + t;
+    const int lp = pos / kPage;
+    if (lp >= bt_stride || q_start + t >= total_q) continue;
+    const int page = bt[(size_t)b * bt_stride + lp];
+    if (page < 0 || page >= num_pages) continue;
+    const size_t src = ((size_t)(q_start + t) * num_kv_heads + h) * chunks_per_row + c;
+    const size_t dst = (((size_t)page * num_kv_heads + h) * kPage + (pos % kPage)) * chunks_per_row + c;
+    k_pool[dst] = k_new[src];
+    v_pool[dst] = v_new[src];
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Planner: one workgroup validates the device-resident lengths against the host bounds and
+// builds the work list (prefill q-tiles, then decode page-range splits), so no host sync is
+// needed.  Writes the header, per-sequence records and entries; zeroes the work counter.
+// ------------------------------------------------------------------------------------------------
+constexpr int kPlanThreads = 1024;
+
+__global__ __launch_bounds__(kPlanThreads) void plan_kernel(
+    PlanParams p, const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ cu,
+    int32_t* __restrict__ hdr, SeqInfo* __restrict__ seqinfo, int32_t* __restrict__ split_base,
+    int2* __restrict__ entries) {
+  __shared__ int s_err;
+  __shared__ long long s_scan[kPlanThreads];
+  __shared__ long long s_carry;
+  const int tid = threadIdx.x;
+  if (tid == 0) { s_err = 0; s_carry = 0; }
+  __syncthreads();
+  // pass 1: validate every sequence
+  for (int b = tid; b < p.batch; b += kPlanThreads) {
+    const int q_start = cu ? cu[b] : b;
+    const int q_len = cu ? cu[b + 1] - q_start : 1;
+    const int ctx = ctx_lens[b];
+    const long long kv = (long long)ctx + q_len;
+    bool bad = q_len < 0 || ctx < 0 || q_start < 0 || q_len > p.max_q_len ||
+               (long long)q_start + q_len > p.total_q || kv > p.max_kv_len ||
+               (kv + kPage - 1) / kPage > p.bt_stride;
+    if (p.mode == kModeDecode && q_len != 1) bad = true;
+    if (bad) atomicOr(&s_err, 1);
+  }
+  __syncthreads();
+  if (s_err) {
+    if (tid == 0) {
+      hdr[kHdrCounter] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
+      hdr[kHdrError] = 1; hdr[kHdrNumItems] = 0;
+    }
+    return;
+  }
+  // pass 2: per-sequence counts, block-wide exclusive scan (prefill count in the low 32 bits,
+  // decode count in the high 32 bits), emit entries
+  for (int base = 0; base < p.batch; base += kPlanThreads) {
+    const int b = base + tid;
+    int n_pre = 0, n_dec = 0, kind = kSeqNone, q_start = 0, q_len = 0, ctx = 0;
+    if (b < p.batch) {
+      q_start = cu ? cu[b] : b;
+      q_len = cu ? cu[b + 1] - q_start : 1;
+      ctx = ctx_lens[b];
+      if (q_len > 0) {
+        const bool dec = p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1);
+        if (dec) {
+          const int pages = (ctx + q_len + kPage - 1) / kPage;
+          kind = kSeqDecode;
+          n_dec = (pages + p.pages_per_split - 1) / p.pages_per_split;
+        } else {
+          kind = kSeqPrefill;
+          n_pre = (q_len + p.tokens_per_tile - 1) / p.tokens_per_tile;
+        }
+      }
+    }
+    const long long v = (long long)n_pre | ((long long)n_dec << 32);
+    s_scan[tid] = v;
+    __syncthreads();
+    for (int off = 1; off < kPlanThreads; off <<= 1) {
+      const long long add = tid >= off ? s_scan[tid - off] : 0;
+      __syncthreads();
+      s_scan[tid] += add;
+      __syncthreads();
+    }
+    const long long incl = s_scan[tid] + s_carry;
+    const long long excl = incl - v;
+    const int pre_off = (int)(excl & 0xffffffffLL);
+    const int dec_off = (int)(excl >> 32);
+    if (b < p.batch) {
+      seqinfo[b] = SeqInfo{q_start, q_len, ctx, kind | (n_dec << 4)};
+      split_base[b] = dec_off;
+      // prefill tiles, last (longest) tile first
+      for (int t = 0; t < n_pre; ++t)
+        if (pre_off + t < p.max_pre) entries[pre_off + t] = make_int2(b, n_pre - 1 - t);
+      for (int s = 0; s < n_dec; ++s)
+        if (dec_off + s < p.max_dec) entries[p.max_pre + dec_off + s] = make_int2(b, s);
+    }
+    __syncthreads();
+    if (tid == kPlanThreads - 1) s_carry = incl;
+    __syncthreads();
+  }
+  if (tid == 0) {
+    const int n_pre = (int)(s_carry & 0xffffffffLL);
+    const int n_dec = (int)(s_carry >> 32);
+    const bool over = n_pre > p.max_pre || n_dec > p.max_dec;
+    hdr[kHdrCounter] = 0;
+    hdr[kHdrNumPre] = over ? 0 : n_pre;
+    hdr[kHdrNumDec] = over ? 0 : n_dec;
+    hdr[kHdrError] = over ? 2 : 0;
+    hdr[kHdrNumItems] = over ? 0 : (n_pre + n_dec) * p.num_kv_heads;
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Prefill-append work item: one (sequence, kv-head g, q-tile).  The tile holds 256 q-rows =
+// tokens_per_tile tokens x G heads of the group (row rho -> token rho / G, head rho % G), so every
+// staged K/V byte is shared by the whole group.  Wave w owns rows [32w, 32w+32).
+//   S^T (keys x rows) = K . Q^T     (32x32x16 MFMA: A = K tile from LDS, B = Q^T in registers)
+//   O^T (dims x rows) += V^T . P^T  (A = V^T via LDS transpose reads, B = P^T from S^T registers)
+// Each lane owns one q-row (l%32) for both products, so the softmax row statistics are
+// lane-local apart from one exchange with lane l^32, which holds the row's other keys.
+// ------------------------------------------------------------------------------------------------
+template <int D>
+__device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile, int g, char* smem) {
+  constexpr int KS = Lds<D>::kStride, VS = Lds<D>::vStride;
+  constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
+  constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
+  constexpr int CPR = D / 8;                        // 16-byte chunks per K/V row
+  constexpr int NCH = kKeysPerStage * CPR / kThreads;  // chunks per thread per tensor per stage
+  static_assert(NCH >= 1 && kKeysPerStage * CPR == NCH * kThreads, "staging split");
+  char* kbuf0 = smem;
+  char* vbuf0 = smem + 2 * kKeysPerStage * KS;
+
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, half = lane >> 5;
+  const SeqInfo si = a.seqinfo[b];
+  const int G = a.group;
+  const int t0 = tile * a.tokens_per_tile;
+  const int t_end = min(t0 + a.tokens_per_tile, si.q_len);
+  const int ctx = si.ctx_len;
+  const int kv_needed = ctx + t_end;
+  const int rho = 32 * w + (lane & 31);
+  const int tok = t0 + rho / G;
+  const int hh = rho - (rho / G) * G;
+  const int h = g * G + hh;
+  const bool row_ok = tok < t_end;
+  const int row_limit = ctx + tok;                  // last visible key of this row
+  const int wave_min_limit = ctx + t0 + (32 * w) / G;
+  const int H_q = a.num_q_heads, H_kv = a.num_kv_heads;
+  const size_t head_stride = (size_t)kPage * D;     // elements per (page, kv-head) block
+  const float c = a.scale_log2;
+
+  bf16x8 qop[KB];
+  {
+    const uint16_t* qrow = a.q + ((size_t)(si.q_start + (row_ok ? tok : t0)) * H_q + h) * D + 8 * half;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qop[kb] = row_ok ? as_bf16x8(ld16(qrow + 16 * kb)) : zero_bf16x8();
+  }
+
+  f32x16 oacc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[mb][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int n_steps = (kv_needed + kKeysPerStage - 1) / kKeysPerStage;
+  const int32_t* bt_row = a.block_table + (size_t)b * a.bt_stride;
+
+  u32x4 kreg[NCH], vreg[NCH];
+  auto load_stage = [&](int step) {
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int cidx = threadIdx.x + i * kThreads;
+      const int kk = cidx / CPR, dc = cidx - kk * CPR;
+      const int j = step * kKeysPerStage + kk;
+      if (j < kv_needed) {
+        const int page = clamp_page(bt_row[j / kPage], a.num_pages);
+        const size_t off = ((size_t)page * H_kv + g) * head_stride + (size_t)(j % kPage) * D + dc * 8;
+        kreg[i] = ld16(a.k_pool + off);
+        vreg[i] = ld16(a.v_pool + off);
+      } else {
+        kreg[i] = u32x4{0u, 0u, 0u, 0u};
+        vreg[i] = u32x4{0u, 0u, 0u, 0u};
+      }
+    }
+  };
+  auto store_stage = [&](int buf) {
+    char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
+    char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
+#pragma unroll
+    for (int i = 0; i < NCH; ++i) {
+      const int cidx = threadIdx.x + i * kThreads;
+      const int kk = cidx / CPR, dc = cidx - kk * CPR;
+      *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = kreg[i];
+      *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = vreg[i];
+    }
+  };
+
+  load_stage(0);
+  store_stage(0);
+  __syncthreads();
+  for (int step = 0; step < n_steps; ++step) {
+    const int buf = step & 1;
+    if (step + 1 < n_steps) load_stage(step + 1);
+    const char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
+    const char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
+    const int k0 = step * kKeysPerStage;
+
+    // S^T = K Q^T for two 32-key sub-tiles
+    f32x16 s[2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
+#pragma unroll
+      for (int kb = 0; kb < KB; ++kb) {
+        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2);
+        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], s[st], 0, 0, 0);
+      }
+    }
+    // causal mask (only on steps that reach past some row's last visible key)
+    if (k0 + kKeysPerStage - 1 > wave_min_limit) {
+#pragma unroll
+      for (int st = 0; st < 2; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + 32 * st + (r & 3) + 8 * (r >> 2) + 4 * half;
+          if (key > row_limit) s[st][r] = -INFINITY;
+        }
+    }
+    // online softmax (base 2)
+    float mx = s[0][0];
+#pragma unroll
+    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * c);
+    const float alpha = fexp2(m_run - m_new);
+    float psum = 0.f;
+    bf16x8 pop[2][2];
+#pragma unroll
+    for (int st = 0; st < 2; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
+        psum += pv;
+        pop[st][r >> 3][r & 7] = (__bf16)pv;
+      }
+    l_run = l_run * alpha + psum;
+    if (__ballot(alpha != 1.0f)) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
+    }
+    m_run = m_new;
+    // O^T += V^T P^T
+    {
+      const int gi = lane >> 4, j = lane & 15;
+      const int krow = 4 * (gi >> 1) + (j >> 2);
+      const int dcol = 16 * (gi & 1) + 4 * (j & 3);
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            const int off = (32 * st + 16 * kk + krow) * VS + (32 * mb + dcol) * 2;
+            const i16x4 v0 = lds_read_tr(vb_, off);
+            const i16x4 v1 = lds_read_tr(vb_, off + 8 * VS);
+            oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(concat_tr(v0, v1), pop[st][kk], oacc[mb], 0, 0, 0);
+          }
+    }
+    if (step + 1 < n_steps) store_stage(buf ^ 1);
+    __syncthreads();
+  }
+
+  // epilogue: combine the two half-row sums, normalise, store bf16 O and fp32 LSE
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (row_ok) {
+    const float inv = 1.0f / l_tot;
+    uint16_t* orow = a.out + ((size_t)(si.q_start + tok) * H_q + h) * D;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int dim = 32 * mb + 8 * rq + 4 * half;
+        u32x2 pk;
+        pk[0] = (uint32_t)bf16_bits(oacc[mb][4 * rq + 0] * inv) | ((uint32_t)bf16_bits(oacc[mb][4 * rq + 1] * inv) << 16);
+        pk[1] = (uint32_t)bf16_bits(oacc[mb][4 * rq + 2] * inv) | ((uint32_t)bf16_bits(oacc[mb][4 * rq + 3] * inv) << 16);
+        *reinterpret_cast<u32x2*>(orow + dim) = pk;
+      }
+    if (half == 0 && a.lse) a.lse[(size_t)(si.q_start + tok) * H_q + h] = (m_run + flog2(l_tot)) * kLn2;
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Decode work item: one (sequence, kv-head g, split of pages_per_split pages).  The G q-heads of
+// the group are the 16 columns of 16x16x32 MFMAs (columns >= G are zero), so each K/V byte is
+// loaded once for the whole group.  Wave w takes page pairs w, w+8, ... of the split:
+//   S^T (16 keys x heads) = K_page . Q^T          (A = K straight from global, 16 B per lane)
+//   O^T (dims x heads)   += V^T . P^T over 32 keys (A = V^T via the wave's LDS slice)
+// The 8 waves' partial softmax states are merged through LDS; a sequence with one split writes
+// its output directly, otherwise the (o~, m, l) partial goes to the workspace.
+// ------------------------------------------------------------------------------------------------
+template <int D>
+__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, char* smem) {
+  constexpr int VS = Lds<D>::vStride;
+  constexpr int KB = D / 32;                 // 32-wide k blocks of the QK product
+  constexpr int MB = D / 16;                 // 16-wide dim blocks of the PV product
+  constexpr int CPR = D / 8;
+  constexpr int VCH = 2 * kPage * CPR / 64;  // V chunks per lane per page pair
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int gi = lane >> 4, hh = lane & 15;
+  const SeqInfo si = a.seqinfo[b];
+  const int G = a.group, H_q = a.num_q_heads, H_kv = a.num_kv_heads;
+  const int kv = si.ctx_len + si.q_len;
+  const int n_pages = (kv + kPage - 1) / kPage;
+  const int p_begin = split * a.pages_per_split;
+  const int p_end = min(p_begin + a.pages_per_split, n_pages);
+  const int n_pairs = (p_end - p_begin + 1) / 2;
+  const bool head_ok = hh < G;
+  const size_t head_stride = (size_t)kPage * D;
+  const float c = a.scale_log2;
+  const int32_t* bt_row = a.block_table + (size_t)b * a.bt_stride;
+  char* vbuf = smem + w * 32 * VS;
+
+  bf16x8 qop[KB];
+  {
+    const uint16_t* qrow = a.q + ((size_t)si.q_start * H_q + g * G + (head_ok ? hh : 0)) * D + 8 * gi;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qop[kb] = head_ok ? as_bf16x8(ld16(qrow + 32 * kb)) : zero_bf16x8();
+  }
+  f32x4 oacc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) oacc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float m_run = -INFINITY, l_run = 0.f;
+
+  for (int pi = w; pi < n_pairs; pi += kWaves) {
+    const int pa = p_begin + 2 * pi;
+    const int pb = pa + 1;
+    const bool pb_ok = pb < p_end;
+    const int phys_a = clamp_page(bt_row[pa], a.num_pages);
+    const int phys_b = pb_ok ? clamp_page(bt_row[pb], a.num_pages) : phys_a;
+    const uint16_t* kpa = a.k_pool + ((size_t)phys_a * H_kv + g) * head_stride;
+    const uint16_t* kpb = a.k_pool + ((size_t)phys_b * H_kv + g) * head_stride;
+    bf16x8 ka[KB], kbv[KB];
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      const int off = hh * D + 32 * kb + 8 * gi;
+      ka[kb] = as_bf16x8(ld16(kpa + off));
+      kbv[kb] = pb_ok ? as_bf16x8(ld16(kpb + off)) : zero_bf16x8();
+    }
+    // V of both pages -> this wave's LDS slice (rows 0..15 page a, 16..31 page b); keys past the
+    // sequence end are stored as zeros so they contribute nothing to P.V.
+#pragma unroll
+    for (int i = 0; i < VCH; ++i) {
+      const int cidx = i * 64 + lane;
+      const int pg = cidx / (kPage * CPR);
+      const int within = cidx - pg * (kPage * CPR);
+      const int key = within / CPR, dc = within - key * CPR;
+      const int keyidx = (pa + pg) * kPage + key;
+      const bool ok = (pg == 0 || pb_ok) && keyidx < kv;
+      u32x4 v = u32x4{0u, 0u, 0u, 0u};
+      if (ok) v = ld16(a.v_pool + ((size_t)(pg ? phys_b : phys_a) * H_kv + g) * head_stride + within * 8);
+      *reinterpret_cast<u32x4*>(vbuf + (pg * kPage + key) * VS + dc * 16) = v;
+    }
+    f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) {
+      sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kb], qop[kb], sa, 0, 0, 0);
+      sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kbv[kb], qop[kb], sb, 0, 0, 0);
+    }
+    // mask keys past the end of the sequence / split
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      if (pa * kPage + 4 * gi + r >= kv) sa[r] = -INFINITY;
+      if (!pb_ok || pb * kPage + 4 * gi + r >= kv) sb[r] = -INFINITY;
+    }
+    float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])), fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float m_new = fmaxf(m_run, mx * c);
+    const float alpha = fexp2(m_run - m_new);
+    bf16x8 pop;
+    float psum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const float p0 = fexp2(__builtin_fmaf(sa[r], c, -m_new));
+      const float p1 = fexp2(__builtin_fmaf(sb[r], c, -m_new));
+      psum += p0 + p1;
+      pop[r] = (__bf16)p0;
+      pop[4 + r] = (__bf16)p1;
+    }
+    l_run = l_run * alpha + psum;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) oacc[mb] *= alpha;
+    m_run = m_new;
+    // the V slice was written by this wave; order the LDS accesses within the wave
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    {
+      const int j = lane & 15;
+      const int off0 = (4 * gi + (j >> 2)) * VS + 4 * (j & 3) * 2;
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const i16x4 v0 = lds_read_tr(vbuf, off0 + 32 * mb);
+        const i16x4 v1 = lds_read_tr(vbuf, off0 + 32 * mb + kPage * VS);
+        oacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(concat_tr(v0, v1), pop, oacc[mb], 0, 0, 0);
+      }
+    }
+    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+    __builtin_amdgcn_wave_barrier();
+    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+  }
+  // each head's four lane groups hold different keys: sum their l
+  l_run += __shfl_xor(l_run, 16);
+  l_run += __shfl_xor(l_run, 32);
+
+  // merge the 8 waves' states through LDS (reuses the V slices)
+  __syncthreads();
+  float* mo = reinterpret_cast<float*>(smem);                 // [wave][8 heads][D]
+  float* mm = mo + kWaves * 8 * D;                            // [wave][8]
+  float* ml = mm + kWaves * 8;                                // [wave][8]
+  if (head_ok) {
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+      *reinterpret_cast<f32x4*>(mo + (w * 8 + hh) * D + 16 * mb + 4 * gi) = oacc[mb];
+    if (gi == 0) { mm[w * 8 + hh] = m_run; ml[w * 8 + hh] = l_run; }
+  }
+  __syncthreads();
+  const int n_splits = si.kind >> 4;
+  for (int t = threadIdx.x; t < G * D; t += kThreads) {
+    const int head = t / D, dim = t - head * D;
+    float M = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, mm[ww * 8 + head]);
+    float L = 0.f, o = 0.f;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) {
+      const float f = fexp2(mm[ww * 8 + head] - M);
+      L += f * ml[ww * 8 + head];
+      o += f * mo[(ww * 8 + head) * D + dim];
+    }
+    const int hq = g * G + head;
+    if (n_splits == 1) {
+      a.out[((size_t)si.q_start * H_q + hq) * D + dim] = bf16_bits(o / L);
+      if (dim == 0 && a.lse) a.lse[(size_t)si.q_start * H_q + hq] = (M + flog2(L)) * kLn2;
+    } else {
+      const size_t pidx = (size_t)(a.split_base[b] + split) * H_q + hq;
+      a.part_o[pidx * D + dim] = o;
+      if (dim == 0) { a.part_ml[2 * pidx] = M; a.part_ml[2 * pidx + 1] = L; }
+    }
+  }
+  __syncthreads();
+}
+
+// ------------------------------------------------------------------------------------------------
+// Persistent attention kernel: workgroups pull items (entry x kv-head) from the planner's list
+// with an atomic counter; prefill tiles come first (largest work), decode splits fill the tail.
+// ------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a, int max_pre) {
+  __shared__ __attribute__((aligned(16))) char smem[Lds<D>::bytes];
+  __shared__ int s_item;
+  const int n_items = a.ws_hdr[kHdrNumItems];
+  const int n_pre = a.ws_hdr[kHdrNumPre];
+  const int H_kv = a.num_kv_heads;
+  for (;;) {
+    if (threadIdx.x == 0) s_item = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+    __syncthreads();
+    const int item = s_item;
+    __syncthreads();
+    if (item >= n_items) break;
+    const int e = item / H_kv;
+    const int g = item - e * H_kv;
+    if (e < n_pre) {
+      const int2 en = a.entries[e];
+      prefill_tile<D>(a, en.x, en.y, g, smem);
+    } else {
+      const int2 en = a.entries[max_pre + (e - n_pre)];
+      decode_split<D>(a, en.x, en.y, g, smem);
+    }
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Split merge: one wave per (sequence, q-head) with more than one split.  The maximum of the
+// split maxima is found with a wavefront shuffle reduction; then
+//   o = sum_s 2^(m_s - m*) o~_s / sum_s 2^(m_s - m*) l_s,   lse = (m* + log2 l*) ln 2.
+// ------------------------------------------------------------------------------------------------
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(AttnArgs a, int batch) {
+  const int lane = threadIdx.x & 63;
+  const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int H_q = a.num_q_heads;
+  if (wid >= batch * H_q) return;
+  if (a.ws_hdr[kHdrError] != 0) return;
+  const int b = wid / H_q, h = wid - (wid / H_q) * H_q;
+  const SeqInfo si = a.seqinfo[b];
+  const int ns = si.kind >> 4;
+  if ((si.kind & 15) != kSeqDecode || ns <= 1) return;
+  const size_t base = (size_t)a.split_base[b];
+  float M = -INFINITY;
+  for (int s = lane; s < ns; s += 64) M = fmaxf(M, a.part_ml[2 * ((base + s) * H_q + h)]);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+  constexpr int PER = D / 64;
+  float acc[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc[i] = 0.f;
+  float L = 0.f;
+  for (int s = 0; s < ns; ++s) {
+    const size_t pidx = (base + s) * H_q + h;
+    const float f = fexp2(a.part_ml[2 * pidx] - M);
+    L += f * a.part_ml[2 * pidx + 1];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[i] += f * a.part_o[pidx * D + lane * PER + i];
+  }
+  const float inv = 1.0f / L;
+  uint16_t* orow = a.out + ((size_t)si.q_start * H_q + h) * D + lane * PER;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) orow[i] = bf16_bits(acc[i] * inv);
+  if (lane == 0 && a.lse) a.lse[(size_t)si.q_start * H_q + h] = (M + flog2(L)) * kLn2;
+}
+
+// ------------------------------------------------------------------------------------------------
+// host launchers
+// ------------------------------------------------------------------------------------------------
+namespace {
+struct DevCache {
+  int num_cu = 0;
+  int occ64 = 0, occ128 = 0;
+};
+DevCache g_cache[64];
+
+DevCache& dev_cache() {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  DevCache& c = g_cache[dev];
+  if (c.num_cu == 0) {
+    hipDeviceProp_t prop;
+    int ncu = 256;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0) ncu = prop.multiProcessorCount;
+    int o64 = 1, o128 = 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o64, attn_kernel<64>, kThreads, 0) != hipSuccess || o64 < 1) o64 = 1;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o128, attn_kernel<128>, kThreads, 0) != hipSuccess || o128 < 1) o128 = 1;
+    c.occ64 = o64;
+    c.occ128 = o128;
+    c.num_cu = ncu;
+  }
+  return c;
+}
+}  // namespace
+
+int device_num_cu() { return dev_cache().num_cu; }
+
+hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                              uint16_t* v_pool, const int32_t* block_table, int bt_stride,
+                              const int32_t* ctx_lens, const int32_t* cu_q_lens, int batch,
+                              int max_q_len, int num_kv_heads, int head_dim, int num_pages,
+                              int total_q, hipStream_t stream) {
+  if (max_q_len <= 0 || batch <= 0) return hipSuccess;
+  dim3 grid((max_q_len + kAppendTokensPerBlock - 1) / kAppendTokensPerBlock, batch);
+  hipLaunchKernelGGL(kv_append_kernel, grid, dim3(256), 0, stream,
+                     reinterpret_cast<const u32x4*>(k_new), reinterpret_cast<const u32x4*>(v_new),
+                     reinterpret_cast<u32x4*>(k_pool), reinterpret_cast<u32x4*>(v_pool), block_table,
+                     bt_stride, ctx_lens, cu_q_lens, num_kv_heads, head_dim / 8, num_pages, total_q);
+  return hipGetLastError();
+}
+
+hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32_t* cu_q_lens,
+                       void* workspace, const WsLayout& lay, hipStream_t stream) {
+  char* ws = static_cast<char*>(workspace);
+  hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, p, ctx_lens, cu_q_lens,
+                     reinterpret_cast<int32_t*>(ws + lay.hdr), reinterpret_cast<SeqInfo*>(ws + lay.seqinfo),
+                     reinterpret_cast<int32_t*>(ws + lay.split_base), reinterpret_cast<int2*>(ws + lay.entries));
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t max_items, int max_pre, hipStream_t stream) {
+  if (max_items <= 0) return hipSuccess;
+  DevCache& c = dev_cache();
+  const int occ = head_dim == 64 ? c.occ64 : c.occ128;
+  int64_t grid = (int64_t)c.num_cu * occ;
+  if (grid > max_items) grid = max_items;
+  if (head_dim == 64)
+    hipLaunchKernelGGL(attn_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, max_pre);
+  else
+    hipLaunchKernelGGL(attn_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, max_pre);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge(const AttnArgs& a, int head_dim, int batch, hipStream_t stream) {
+  const int64_t waves = (int64_t)batch * a.num_q_heads;
+  const unsigned grid = (unsigned)((waves + 3) / 4);
+  if (grid == 0) return hipSuccess;
+  if (head_dim == 64)
+    hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(256), 0, stream, a, batch);
+  else
+    hipLaunchKernelGGL(merge_kernel<128>, dim3(grid), dim3(256), 0, stream, a, batch);
+  return hipGetLastError();
+}
+
+}  // namespace pearl

@@ -1,0 +1,107 @@
+// Internal interface between the C-ABI host layer (api.cpp) and the gfx950 kernels
+// (attn_kernels.hip).  Not installed; callers use include/pearl_attn.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace pearl {
+
+constexpr int kPage = 16;            // tokens per KV page
+constexpr int kThreads = 512;        // threads per attention workgroup (8 waves of 64)
+constexpr int kWaves = kThreads / 64;
+constexpr int kRowsPerTile = 256;    // q-rows (token x head-in-group) per prefill work item
+constexpr int kKeysPerStage = 64;    // keys staged in LDS per prefill step (4 pages)
+constexpr int kMinPagesPerSplit = 16;
+// Compute units assumed when sizing decode splits (MI355X has 256).  A fixed value keeps the
+// workspace size a pure function of the shapes; the launch grid uses the device's real count.
+constexpr int kPlanComputeUnits = 256;
+
+enum Mode : int { kModePrefill = 0, kModeDecode = 1, kModeMixed = 2 };
+
+// Kinds recorded per sequence by the planner.
+enum SeqKind : int { kSeqNone = 0, kSeqPrefill = 1, kSeqDecode = 2 };
+
+// Workspace header (int32 words).
+enum Hdr : int {
+  kHdrCounter = 0,     // dynamic work counter (atomic)
+  kHdrNumPre = 1,      // prefill entries
+  kHdrNumDec = 2,      // decode split entries
+  kHdrError = 3,       // nonzero: a sequence violated the host bounds; nothing is computed
+  kHdrNumItems = 4,    // (pre + dec) * H_kv
+  kHdrWords = 64
+};
+
+// Per-sequence record written by the planner.
+struct SeqInfo {
+  int32_t q_start;   // first row of the sequence in q/out
+  int32_t q_len;     // new tokens
+  int32_t ctx_len;   // cached tokens before the call
+  int32_t kind;      // SeqKind | (n_splits << 4) for decode sequences
+};
+
+// Offsets (bytes) of the workspace regions; all 256-byte aligned.
+struct WsLayout {
+  size_t hdr, seqinfo, split_base, entries, part_o, part_ml, total;
+  int64_t max_pre, max_dec;
+};
+
+struct PlanParams {
+  int mode;
+  int batch;
+  int total_q;
+  int max_q_len;
+  int max_kv_len;
+  int bt_stride;
+  int num_kv_heads;
+  int group;             // G
+  int tokens_per_tile;   // kRowsPerTile / G
+  int pages_per_split;
+  int64_t max_pre;       // capacity of the prefill entry list
+  int64_t max_dec;       // capacity of the decode entry list (and of the partial buffers)
+};
+
+struct AttnArgs {
+  const uint16_t* q;
+  const uint16_t* k_pool;
+  const uint16_t* v_pool;
+  const int32_t* block_table;
+  uint16_t* out;
+  float* lse;                // may be null
+  int32_t* ws_hdr;
+  const SeqInfo* seqinfo;
+  const int32_t* split_base;
+  const int2* entries;
+  float* part_o;
+  float* part_ml;
+  int bt_stride;
+  int num_pages;
+  int num_q_heads;
+  int num_kv_heads;
+  int group;
+  int tokens_per_tile;
+  int pages_per_split;
+  float scale_log2;          // softmax_scale * log2(e)
+};
+
+WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_heads,
+                          int num_kv_heads, int head_dim, int group, int pages_per_split);
+int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu);
+int device_num_cu();
+
+hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
+                            uint16_t* v_pool, const int32_t* block_table, int bt_stride,
+                            const int32_t* ctx_lens, const int32_t* cu_q_lens, int batch,
+                            int max_q_len, int num_kv_heads, int head_dim, int num_pages,
+                            int total_q, hipStream_t stream);
+
+hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32_t* cu_q_lens,
+                       void* workspace, const WsLayout& lay, hipStream_t stream);
+
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t max_items, int max_pre,
+                            hipStream_t stream);
+
+hipError_t launch_merge(const AttnArgs& a, int head_dim, int batch, hipStream_t stream);
+
+}  // namespace pearl

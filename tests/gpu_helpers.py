@@ -1,0 +1,120 @@
+"""Helpers shared by the GPU parity tests: run the HIP path through the C ABI on a synthetic
+case, and run the CPU oracle on the same bytes (whole case or sampled sequences)."""
+from __future__ import annotations
+
+import sys
+from typing import Dict, Iterable, List, Optional, Sequence, Tuple
+
+import numpy as np
+import torch
+
+import oracle
+import paper_2609_35158_amd as pa
+from paper_2609_35158_amd import workloads
+
+# Tolerance for bf16 outputs against the float64 oracle (bf16 inputs/outputs, fp32 accumulation).
+MAX_ABS = 1e-2
+MEAN_ABS = 1e-3
+LSE_ABS = 1e-3
+
+
+def say(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def bits(t: torch.Tensor) -> np.ndarray:
+    return t.detach().contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def dev_lengths(case: workloads.Case):
+    dev = case.q.device
+    ctx = torch.from_numpy(case.ctx_lens.astype(np.int32)).to(dev)
+    cu = torch.from_numpy(case.cu_q_lens.astype(np.int32)).to(dev)
+    return ctx, cu
+
+
+def bounds(case: workloads.Case) -> Tuple[int, int]:
+    max_q = int(case.q_lens.max()) if case.batch else 0
+    max_kv = int(case.kv_lens.max()) if case.batch else 0
+    return max_q, max_kv
+
+
+def gpu_append(case: workloads.Case, decode_layout: bool = False) -> None:
+    ctx, cu = dev_lengths(case)
+    max_q, max_kv = bounds(case)
+    pa.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, ctx,
+                 None if decode_layout else cu, max_q, max_kv)
+
+
+def gpu_attend(case: workloads.Case, mode: str, return_lse: bool = True, max_kv_len: Optional[int] = None):
+    ctx, cu = dev_lengths(case)
+    max_q, max_kv = bounds(case)
+    if max_kv_len is not None:
+        max_kv = max_kv_len
+    if mode == "decode":
+        return pa.decode(case.q, case.k_pool, case.v_pool, case.block_table, ctx, max_kv,
+                         scale=case.scale, return_lse=return_lse)
+    if mode == "prefill":
+        return pa.prefill_append(case.q, case.k_pool, case.v_pool, case.block_table, ctx, cu, max_q,
+                                 max_kv, scale=case.scale, return_lse=return_lse)
+    if mode == "mixed":
+        return pa.mixed(case.q, case.k_pool, case.v_pool, case.block_table, ctx, cu, max_q, max_kv,
+                        scale=case.scale, return_lse=return_lse)
+    raise ValueError(mode)
+
+
+def oracle_full(case: workloads.Case, k_pool_bits=None, v_pool_bits=None):
+    kp = bits(case.k_pool) if k_pool_bits is None else k_pool_bits
+    vp = bits(case.v_pool) if v_pool_bits is None else v_pool_bits
+    return oracle.attention(bits(case.q), kp, vp, case.block_table.cpu().numpy(), case.ctx_lens,
+                            case.cu_q_lens, case.scale)
+
+
+def oracle_sampled(case: workloads.Case, seqs: Sequence[int], tokens: Optional[Dict[int, List[int]]] = None,
+                   heads: Optional[Sequence[int]] = None):
+    """Oracle on a subset of sequences: gather only their pages (compact pool, remapped block
+    table) so multi-GB pools need not be copied to the host."""
+    bt = case.block_table.cpu().numpy()
+    npages = (case.kv_lens + 15) // 16
+    rows, cols = [], []
+    for b in seqs:
+        rows.append(bt[b, :npages[b]])
+    uniq = np.unique(np.concatenate(rows)) if rows else np.zeros(0, np.int64)
+    remap = {int(p): i for i, p in enumerate(uniq)}
+    idx = torch.from_numpy(uniq.astype(np.int64)).to(case.k_pool.device)
+    kp = bits(case.k_pool.index_select(0, idx))
+    vp = bits(case.v_pool.index_select(0, idx))
+    sub_bt = np.zeros((len(seqs), max(1, int(npages[list(seqs)].max()))), np.int32)
+    for i, b in enumerate(seqs):
+        sub_bt[i, :npages[b]] = [remap[int(p)] for p in bt[b, :npages[b]]]
+    cu = case.cu_q_lens
+    q_all = bits(case.q)
+    # per selected sequence, build its own rows
+    out_o, out_l = {}, {}
+    for i, b in enumerate(seqs):
+        n = int(case.q_lens[b])
+        qb = q_all[cu[b]:cu[b] + n]
+        sel = None if tokens is None else {0: tokens[b]}
+        o, l = oracle.attention(qb, kp, vp, sub_bt[i:i + 1], case.ctx_lens[b:b + 1],
+                                np.array([0, n], np.int32), case.scale, heads=heads, tokens=sel)
+        out_o[b], out_l[b] = o, l
+    return out_o, out_l
+
+
+def assert_close(gpu_o_bits: np.ndarray, ref_o: np.ndarray, gpu_lse: Optional[np.ndarray] = None,
+                 ref_lse: Optional[np.ndarray] = None, what: str = "") -> dict:
+    st = oracle.compare(gpu_o_bits, ref_o)
+    say("   parity %s: n=%d max_abs=%.3e mean_abs=%.3e max_ulp=%.1f" % (what, st["n"], st["max_abs"],
+                                                                          st["mean_abs"], st["max_ulp"]))
+    assert st["n"] > 0, "nothing compared"
+    assert st["nonfinite_gpu"] == 0, "non-finite GPU outputs (%s)" % what
+    assert st["max_abs"] <= MAX_ABS, "max_abs %.3e > %.1e (%s)" % (st["max_abs"], MAX_ABS, what)
+    assert st["mean_abs"] <= MEAN_ABS, "mean_abs %.3e > %.1e (%s)" % (st["mean_abs"], MEAN_ABS, what)
+    if gpu_lse is not None and ref_lse is not None:
+        m = np.isfinite(ref_lse)
+        d = np.abs(gpu_lse[m].astype(np.float64) - ref_lse[m])
+        say("   lse %s: max_abs=%.3e" % (what, d.max() if d.size else 0.0))
+        assert np.all(np.isfinite(gpu_lse[m]))
+        assert d.size == 0 or d.max() <= LSE_ABS, "lse max_abs %.3e (%s)" % (d.max(), what)
+    return st
