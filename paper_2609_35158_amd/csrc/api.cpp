@@ -167,7 +167,8 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   const int64_t max_items = (pl.lay.max_pre + pl.lay.max_dec) * s->num_kv_heads;
   e = record_before(hs);
   if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
-  e = launch_attention(a, s->head_dim, max_items, (int)pl.lay.max_pre, hs);
+  const int kinds = mode == kModePrefill ? 1 : (mode == kModeDecode ? 2 : 3);
+  e = launch_attention(a, s->head_dim, kinds, max_items, (int)pl.lay.max_pre, hs);
   if (e != hipSuccess) return fail(PEARL_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
   e = record_after(hs);
   if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
@@ -198,7 +199,7 @@ int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_
   int64_t pps = cdiv((int64_t)batch * num_kv_heads * max_pages, target);
   pps = std::max<int64_t>(pps, kMinPagesPerSplit);
   pps = cdiv(pps, 16) * 16;
-  if (pps > (int64_t)1 << 20) pps = (int64_t)1 << 20;
+  if (pps > kMaxPagesPerSplit) pps = kMaxPagesPerSplit;
   return (int)pps;
 }
 

@@ -72,7 +72,7 @@ template <int D> struct Lds {
   static constexpr int kStride = D * 2 + 16;
   static constexpr int vStride = D * 2 + 32;
   static constexpr int prefill_bytes = 2 * kKeysPerStage * (kStride + vStride);
-  static constexpr int decode_v_bytes = kWaves * 32 * vStride;
+  static constexpr int decode_v_bytes = kWaves * 2 * (2 * kPage * D * 2);   // per-wave double buffer
   static constexpr int merge_bytes = kWaves * 8 * D * 4 + 2 * kWaves * 8 * 4;
   static constexpr int decode_bytes = decode_v_bytes > merge_bytes ? decode_v_bytes : merge_bytes;
   static constexpr int bytes = prefill_bytes > decode_bytes ? prefill_bytes : decode_bytes;
@@ -130,6 +130,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __shared__ long long s_carry;
   const int tid = threadIdx.x;
   if (tid == 0) { s_err = 0; s_carry = 0; }
+  if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
   __syncthreads();
   // pass 1: validate every sequence
   for (int b = tid; b < p.batch; b += kPlanThreads) {
@@ -398,127 +399,197 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
 // Decode work item: one (sequence, kv-head g, split of pages_per_split pages).  The G q-heads of
 // the group are the 16 columns of 16x16x32 MFMAs (columns >= G are zero), so each K/V byte is
 // loaded once for the whole group.  Wave w takes page pairs w, w+8, ... of the split:
-//   S^T (16 keys x heads) = K_page . Q^T          (A = K straight from global, 16 B per lane)
-//   O^T (dims x heads)   += V^T . P^T over 32 keys (A = V^T via the wave's LDS slice)
-// The 8 waves' partial softmax states are merged through LDS; a sequence with one split writes
-// its output directly, otherwise the (o~, m, l) partial goes to the workspace.
+//   S^T (16 keys x heads) = K_page . Q^T          (A = K straight from HBM into registers)
+//   O^T (dims x heads)   += V^T . P^T over 32 keys (A = V^T read transposed from LDS)
+// V travels HBM -> LDS with 16-byte LDS-DMA loads (no VGPRs, no LDS store instructions) into a
+// per-wave double buffer; K is double-buffered in registers, so the next pair's loads are in
+// flight while the current pair is consumed.  Every load is unconditional: addresses stay inside
+// the split's own pages, and V rows of keys past the sequence end are fetched from a zeroed block
+// of the workspace so they add nothing to P.V (their scores are masked to -inf).  The 8 waves'
+// partial softmax states are merged through LDS; a sequence with one split writes its output
+// directly, otherwise the (o~, m, l) partial goes to the workspace.
+//
+// V buffer layout: 32 rows (keys of the pair) x D/8 16-byte chunks, unpadded; chunk c of row r is
+// stored at chunk slot c ^ swz(r), which spreads the transpose reads over all LDS banks.
 // ------------------------------------------------------------------------------------------------
+template <int D> struct DecodeK {
+  static constexpr int KB = D / 32;                 // 32-wide k blocks of the QK product
+  u32x4 ka[KB], kb[KB];
+};
+
+template <int D> struct VTile {
+  static constexpr int CPR = D / 8;                 // 16-byte chunks per key row
+  static constexpr int ROWB = D * 2;                // bytes per key row
+  static constexpr int RPI = 64 / CPR;              // rows written by one 64-lane DMA instruction
+  static constexpr int PAIR_BYTES = 2 * kPage * ROWB;
+  static constexpr int NDMA = 2 * kPage / RPI;      // DMA instructions per page pair
+  __device__ static __forceinline__ int swz(int r) {
+    return (((r & 3) << 2) | (((r >> 2) & 1) << 1)) & (CPR - 1);
+  }
+  // byte offset of (row r, 4-element group starting at dim d0) inside the buffer
+  __device__ static __forceinline__ int off(int r, int d0) {
+    return r * ROWB + (((d0 >> 3) ^ swz(r)) << 4) + ((d0 >> 2) & 1) * 8;
+  }
+};
+
+__device__ __forceinline__ void lds_dma16(const void* g, char* lds_base) {
+  __builtin_amdgcn_global_load_lds(g, (LDS_AS void*)((LDS_AS char*)(lds_base)), 16, 0, 0);
+}
+
 template <int D>
-__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, char* smem) {
-  constexpr int VS = Lds<D>::vStride;
-  constexpr int KB = D / 32;                 // 32-wide k blocks of the QK product
-  constexpr int MB = D / 16;                 // 16-wide dim blocks of the PV product
-  constexpr int CPR = D / 8;
-  constexpr int VCH = 2 * kPage * CPR / 64;  // V chunks per lane per page pair
+__device__ __forceinline__ void decode_issue(const AttnArgs& a, const int* s_pages, int p_begin, int p_end,
+                                             int g, int kv, int pi, DecodeK<D>& K, char* vdst) {
+  using VT = VTile<D>;
+  const int lane = threadIdx.x & 63, gi = lane >> 4, hh = lane & 15;
+  const int pa = p_begin + 2 * pi;
+  const bool pb_ok = pa + 1 < p_end;
+  const int pb = pb_ok ? pa + 1 : pa;               // a missing second page re-reads the first
+  const int phys_a = s_pages[pa - p_begin];
+  const int phys_b = s_pages[pb - p_begin];
+  const size_t head_stride = (size_t)kPage * D;
+  const size_t ga = ((size_t)phys_a * a.num_kv_heads + g) * head_stride;
+  const size_t gb = ((size_t)phys_b * a.num_kv_heads + g) * head_stride;
+#pragma unroll
+  for (int kb = 0; kb < DecodeK<D>::KB; ++kb) {
+    const int off = hh * D + 32 * kb + 8 * gi;
+    K.ka[kb] = ld16(a.k_pool + ga + off);
+    K.kb[kb] = ld16(a.k_pool + gb + off);
+  }
+  const uint16_t* zero = reinterpret_cast<const uint16_t*>(a.ws_hdr + kHdrZero);
+#pragma unroll
+  for (int i = 0; i < VT::NDMA; ++i) {
+    const int r = i * VT::RPI + lane / VT::CPR;     // key row of the pair written by this lane
+    const int slot_c = lane % VT::CPR;              // chunk slot this lane fills
+    const int c = slot_c ^ VT::swz(r);              // global chunk stored there
+    const int pg = r >> 4, key = r & 15;            // pg is the same for every lane of a given i
+    const bool ok = (pg == 0 || pb_ok) && (pa + pg) * kPage + key < kv;
+    const uint16_t* src = ok ? a.v_pool + (pg ? gb : ga) + key * D + c * 8 : zero;
+    lds_dma16(src, vdst + i * 1024);
+  }
+}
+
+template <int D>
+__device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<D>& K, int pa, bool pb_ok,
+                                               int kv, const bf16x8* qop, f32x4* oacc, float& m_run,
+                                               float& l_run, const char* vbuf) {
+  using VT = VTile<D>;
+  constexpr int KB = DecodeK<D>::KB;
+  constexpr int MB = D / 16;                       // 16-wide dim blocks of the PV product
+  const int lane = threadIdx.x & 63, gi = lane >> 4;
+  const float c = a.scale_log2;
+  const int pb = pa + 1;
+  f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) {
+    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(K.ka[kb]), qop[kb], sa, 0, 0, 0);
+    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(K.kb[kb]), qop[kb], sb, 0, 0, 0);
+  }
+  // mask keys past the end of the sequence / split (a select, so stray bit patterns never leak)
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    sa[r] = (pa * kPage + 4 * gi + r < kv) ? sa[r] : -INFINITY;
+    sb[r] = (pb_ok && pb * kPage + 4 * gi + r < kv) ? sb[r] : -INFINITY;
+  }
+  float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])), fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  const float m_new = fmaxf(m_run, mx * c);
+  const float alpha = fexp2(m_run - m_new);
+  bf16x8 pop;
+  float psum = 0.f;
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const float p0 = fexp2(__builtin_fmaf(sa[r], c, -m_new));
+    const float p1 = fexp2(__builtin_fmaf(sb[r], c, -m_new));
+    psum += p0 + p1;
+    pop[r] = (__bf16)p0;
+    pop[4 + r] = (__bf16)p1;
+  }
+  l_run = l_run * alpha + psum;
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb) oacc[mb] *= alpha;
+  m_run = m_new;
+  {
+    const int j = lane & 15;
+    const int r0 = 4 * gi + (j >> 2);              // rows of page a; page b rows are +16
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int d0 = 16 * mb + 4 * (j & 3);
+      const i16x4 v0 = lds_read_tr(vbuf, VT::off(r0, d0));
+      const i16x4 v1 = lds_read_tr(vbuf, VT::off(r0 + kPage, d0));
+      oacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(concat_tr(v0, v1), pop, oacc[mb], 0, 0, 0);
+    }
+  }
+}
+
+// vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
+#define PEARL_VMCNT(n) (((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
+
+template <int D>
+__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, char* smem, int* s_pages) {
+  using VT = VTile<D>;
+  constexpr int MB = D / 16;
+  constexpr int KB = DecodeK<D>::KB;
+  constexpr int PAIR_LOADS = 2 * KB + VT::NDMA;    // vector-memory instructions issued per pair
   const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
   const int gi = lane >> 4, hh = lane & 15;
   const SeqInfo si = a.seqinfo[b];
-  const int G = a.group, H_q = a.num_q_heads, H_kv = a.num_kv_heads;
+  const int G = a.group, H_q = a.num_q_heads;
   const int kv = si.ctx_len + si.q_len;
   const int n_pages = (kv + kPage - 1) / kPage;
   const int p_begin = split * a.pages_per_split;
   const int p_end = min(p_begin + a.pages_per_split, n_pages);
   const int n_pairs = (p_end - p_begin + 1) / 2;
   const bool head_ok = hh < G;
-  const size_t head_stride = (size_t)kPage * D;
-  const float c = a.scale_log2;
+  char* vb0 = smem + w * 2 * VT::PAIR_BYTES;
+  char* vb1 = vb0 + VT::PAIR_BYTES;
+
+  // stage this split's physical page ids once (clamped into the pool)
   const int32_t* bt_row = a.block_table + (size_t)b * a.bt_stride;
-  char* vbuf = smem + w * 32 * VS;
+  for (int i = threadIdx.x; i < p_end - p_begin; i += kThreads) s_pages[i] = clamp_page(bt_row[p_begin + i], a.num_pages);
+  __syncthreads();
 
   bf16x8 qop[KB];
   {
     const uint16_t* qrow = a.q + ((size_t)si.q_start * H_q + g * G + (head_ok ? hh : 0)) * D + 8 * gi;
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) qop[kb] = head_ok ? as_bf16x8(ld16(qrow + 32 * kb)) : zero_bf16x8();
+    for (int kb = 0; kb < KB; ++kb) {
+      const bf16x8 v = as_bf16x8(ld16(qrow + 32 * kb));
+      qop[kb] = head_ok ? v : zero_bf16x8();
+    }
   }
+  DecodeK<D> kA, kB;
+  if (w < n_pairs) decode_issue<D>(a, s_pages, p_begin, p_end, g, kv, w, kA, vb0);
   f32x4 oacc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) oacc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  for (int pi = w; pi < n_pairs; pi += kWaves) {
-    const int pa = p_begin + 2 * pi;
-    const int pb = pa + 1;
-    const bool pb_ok = pb < p_end;
-    const int phys_a = clamp_page(bt_row[pa], a.num_pages);
-    const int phys_b = pb_ok ? clamp_page(bt_row[pb], a.num_pages) : phys_a;
-    const uint16_t* kpa = a.k_pool + ((size_t)phys_a * H_kv + g) * head_stride;
-    const uint16_t* kpb = a.k_pool + ((size_t)phys_b * H_kv + g) * head_stride;
-    bf16x8 ka[KB], kbv[KB];
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      const int off = hh * D + 32 * kb + 8 * gi;
-      ka[kb] = as_bf16x8(ld16(kpa + off));
-      kbv[kb] = pb_ok ? as_bf16x8(ld16(kpb + off)) : zero_bf16x8();
+  for (int pi = w; pi < n_pairs; pi += 2 * kWaves) {
+    // the next pair's loads go out before this pair is consumed
+    const int pj = pi + kWaves;
+    if (pj < n_pairs) {
+      decode_issue<D>(a, s_pages, p_begin, p_end, g, kv, pj, kB, vb1);
+      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));   // this pair's K and V have landed
+    } else {
+      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
     }
-    // V of both pages -> this wave's LDS slice (rows 0..15 page a, 16..31 page b); keys past the
-    // sequence end are stored as zeros so they contribute nothing to P.V.
-#pragma unroll
-    for (int i = 0; i < VCH; ++i) {
-      const int cidx = i * 64 + lane;
-      const int pg = cidx / (kPage * CPR);
-      const int within = cidx - pg * (kPage * CPR);
-      const int key = within / CPR, dc = within - key * CPR;
-      const int keyidx = (pa + pg) * kPage + key;
-      const bool ok = (pg == 0 || pb_ok) && keyidx < kv;
-      u32x4 v = u32x4{0u, 0u, 0u, 0u};
-      if (ok) v = ld16(a.v_pool + ((size_t)(pg ? phys_b : phys_a) * H_kv + g) * head_stride + within * 8);
-      *reinterpret_cast<u32x4*>(vbuf + (pg * kPage + key) * VS + dc * 16) = v;
+    decode_consume<D>(a, kA, p_begin + 2 * pi, p_begin + 2 * pi + 1 < p_end, kv, qop, oacc, m_run, l_run, vb0);
+    if (pj >= n_pairs) break;
+    const int pk = pj + kWaves;
+    if (pk < n_pairs) {
+      decode_issue<D>(a, s_pages, p_begin, p_end, g, kv, pk, kA, vb0);
+      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));
+    } else {
+      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
     }
-    f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) {
-      sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ka[kb], qop[kb], sa, 0, 0, 0);
-      sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kbv[kb], qop[kb], sb, 0, 0, 0);
-    }
-    // mask keys past the end of the sequence / split
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      if (pa * kPage + 4 * gi + r >= kv) sa[r] = -INFINITY;
-      if (!pb_ok || pb * kPage + 4 * gi + r >= kv) sb[r] = -INFINITY;
-    }
-    float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])), fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
-    mx = fmaxf(mx, __shfl_xor(mx, 16));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * c);
-    const float alpha = fexp2(m_run - m_new);
-    bf16x8 pop;
-    float psum = 0.f;
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const float p0 = fexp2(__builtin_fmaf(sa[r], c, -m_new));
-      const float p1 = fexp2(__builtin_fmaf(sb[r], c, -m_new));
-      psum += p0 + p1;
-      pop[r] = (__bf16)p0;
-      pop[4 + r] = (__bf16)p1;
-    }
-    l_run = l_run * alpha + psum;
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) oacc[mb] *= alpha;
-    m_run = m_new;
-    // the V slice was written by this wave; order the LDS accesses within the wave
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-    {
-      const int j = lane & 15;
-      const int off0 = (4 * gi + (j >> 2)) * VS + 4 * (j & 3) * 2;
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const i16x4 v0 = lds_read_tr(vbuf, off0 + 32 * mb);
-        const i16x4 v1 = lds_read_tr(vbuf, off0 + 32 * mb + kPage * VS);
-        oacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(concat_tr(v0, v1), pop, oacc[mb], 0, 0, 0);
-      }
-    }
-    __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-    __builtin_amdgcn_wave_barrier();
-    __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+    decode_consume<D>(a, kB, p_begin + 2 * pj, p_begin + 2 * pj + 1 < p_end, kv, qop, oacc, m_run, l_run, vb1);
   }
   // each head's four lane groups hold different keys: sum their l
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
 
-  // merge the 8 waves' states through LDS (reuses the V slices)
+  // merge the 8 waves' states through LDS (reuses the V buffers)
   __syncthreads();
   float* mo = reinterpret_cast<float*>(smem);                 // [wave][8 heads][D]
   float* mm = mo + kWaves * 8 * D;                            // [wave][8]
@@ -558,30 +629,40 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
 
 // ------------------------------------------------------------------------------------------------
 // Persistent attention kernel: workgroups pull items (entry x kv-head) from the planner's list
-// with an atomic counter; prefill tiles come first (largest work), decode splits fill the tail.
+// with an atomic counter (the next item is claimed while the current one runs); prefill tiles
+// come first (largest work), decode splits fill the tail.
 // ------------------------------------------------------------------------------------------------
-template <int D>
+// kKinds: 1 = prefill tiles only, 2 = decode splits only, 3 = both (mixed batches).
+template <int D, int kKinds>
 __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a, int max_pre) {
   __shared__ __attribute__((aligned(16))) char smem[Lds<D>::bytes];
-  __shared__ int s_item;
+  __shared__ int s_pages[kMaxPagesPerSplit];
+  __shared__ int s_item[2];
   const int n_items = a.ws_hdr[kHdrNumItems];
   const int n_pre = a.ws_hdr[kHdrNumPre];
   const int H_kv = a.num_kv_heads;
-  for (;;) {
-    if (threadIdx.x == 0) s_item = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
-    __syncthreads();
-    const int item = s_item;
-    __syncthreads();
-    if (item >= n_items) break;
+  if (threadIdx.x == 0) s_item[0] = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+  __syncthreads();
+  int slot = 0;
+  int item = s_item[0];
+  while (item < n_items) {
+    if (threadIdx.x == 0) s_item[slot ^ 1] = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
     const int e = item / H_kv;
     const int g = item - e * H_kv;
     if (e < n_pre) {
-      const int2 en = a.entries[e];
-      prefill_tile<D>(a, en.x, en.y, g, smem);
+      if constexpr ((kKinds & 1) != 0) {
+        const int2 en = a.entries[e];
+        prefill_tile<D>(a, en.x, en.y, g, smem);
+      }
     } else {
-      const int2 en = a.entries[max_pre + (e - n_pre)];
-      decode_split<D>(a, en.x, en.y, g, smem);
+      if constexpr ((kKinds & 2) != 0) {
+        const int2 en = a.entries[max_pre + (e - n_pre)];
+        decode_split<D>(a, en.x, en.y, g, smem, s_pages);
+      }
     }
+    __syncthreads();
+    slot ^= 1;
+    item = s_item[slot];
   }
 }
 
@@ -631,8 +712,15 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a, int batch) {
 namespace {
 struct DevCache {
   int num_cu = 0;
-  int occ64 = 0, occ128 = 0;
+  int occ[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};   // [D == 128][kinds]
 };
+
+template <int D, int K>
+int occupancy_of() {
+  int o = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, attn_kernel<D, K>, kThreads, 0) != hipSuccess || o < 1) o = 1;
+  return o;
+}
 DevCache g_cache[64];
 
 DevCache& dev_cache() {
@@ -643,11 +731,8 @@ DevCache& dev_cache() {
     hipDeviceProp_t prop;
     int ncu = 256;
     if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0) ncu = prop.multiProcessorCount;
-    int o64 = 1, o128 = 1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o64, attn_kernel<64>, kThreads, 0) != hipSuccess || o64 < 1) o64 = 1;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o128, attn_kernel<128>, kThreads, 0) != hipSuccess || o128 < 1) o128 = 1;
-    c.occ64 = o64;
-    c.occ128 = o128;
+    c.occ[0][1] = occupancy_of<64, 1>(); c.occ[0][2] = occupancy_of<64, 2>(); c.occ[0][3] = occupancy_of<64, 3>();
+    c.occ[1][1] = occupancy_of<128, 1>(); c.occ[1][2] = occupancy_of<128, 2>(); c.occ[1][3] = occupancy_of<128, 3>();
     c.num_cu = ncu;
   }
   return c;
@@ -679,16 +764,24 @@ hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32
   return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t max_items, int max_pre, hipStream_t stream) {
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t max_items, int max_pre,
+                            hipStream_t stream) {
   if (max_items <= 0) return hipSuccess;
+  if (kinds < 1 || kinds > 3) return hipErrorInvalidValue;
   DevCache& c = dev_cache();
-  const int occ = head_dim == 64 ? c.occ64 : c.occ128;
+  const int occ = c.occ[head_dim == 128 ? 1 : 0][kinds];
   int64_t grid = (int64_t)c.num_cu * occ;
   if (grid > max_items) grid = max_items;
-  if (head_dim == 64)
-    hipLaunchKernelGGL(attn_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, max_pre);
-  else
-    hipLaunchKernelGGL(attn_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, max_pre);
+  const dim3 g((unsigned)grid), blk(kThreads);
+  if (head_dim == 64) {
+    if (kinds == 1) hipLaunchKernelGGL((attn_kernel<64, 1>), g, blk, 0, stream, a, max_pre);
+    else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<64, 2>), g, blk, 0, stream, a, max_pre);
+    else hipLaunchKernelGGL((attn_kernel<64, 3>), g, blk, 0, stream, a, max_pre);
+  } else {
+    if (kinds == 1) hipLaunchKernelGGL((attn_kernel<128, 1>), g, blk, 0, stream, a, max_pre);
+    else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<128, 2>), g, blk, 0, stream, a, max_pre);
+    else hipLaunchKernelGGL((attn_kernel<128, 3>), g, blk, 0, stream, a, max_pre);
+  }
   return hipGetLastError();
 }
 

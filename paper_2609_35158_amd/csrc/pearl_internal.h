@@ -14,6 +14,7 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kRowsPerTile = 256;    // q-rows (token x head-in-group) per prefill work item
 constexpr int kKeysPerStage = 64;    // keys staged in LDS per prefill step (4 pages)
 constexpr int kMinPagesPerSplit = 16;
+constexpr int kMaxPagesPerSplit = 512;   // page ids of one split are staged in LDS
 // Compute units assumed when sizing decode splits (MI355X has 256).  A fixed value keeps the
 // workspace size a pure function of the shapes; the launch grid uses the device's real count.
 constexpr int kPlanComputeUnits = 256;
@@ -30,6 +31,7 @@ enum Hdr : int {
   kHdrNumDec = 2,      // decode split entries
   kHdrError = 3,       // nonzero: a sequence violated the host bounds; nothing is computed
   kHdrNumItems = 4,    // (pre + dec) * H_kv
+  kHdrZero = 32,       // words 32..63: a zeroed 128-byte block (source for keys past the end)
   kHdrWords = 64
 };
 
@@ -99,7 +101,8 @@ hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16
 hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32_t* cu_q_lens,
                        void* workspace, const WsLayout& lay, hipStream_t stream);
 
-hipError_t launch_attention(const AttnArgs& a, int head_dim, int64_t max_items, int max_pre,
+// kinds: 1 = prefill tiles only, 2 = decode splits only, 3 = both.
+hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t max_items, int max_pre,
                             hipStream_t stream);
 
 hipError_t launch_merge(const AttnArgs& a, int head_dim, int batch, hipStream_t stream);
