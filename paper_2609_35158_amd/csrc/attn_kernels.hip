@@ -68,14 +68,17 @@ __device__ __forceinline__ int clamp_page(int p, int num_pages) {
 }
 
 // LDS row strides (bytes) of staged K and V tiles: row = one key, padded against bank conflicts.
-template <int D> struct Lds {
+// NW = waves per workgroup; kinds as in attn_kernel.
+template <int D, int NW, int kKinds> struct Lds {
   static constexpr int kStride = D * 2 + 16;
   static constexpr int vStride = D * 2 + 32;
-  static constexpr int prefill_bytes = 2 * kKeysPerStage * (kStride + vStride);
-  static constexpr int decode_v_bytes = kWaves * 2 * (2 * kPage * D * 2);   // per-wave double buffer
-  static constexpr int merge_bytes = kWaves * 8 * D * 4 + 2 * kWaves * 8 * 4;
-  static constexpr int decode_bytes = decode_v_bytes > merge_bytes ? decode_v_bytes : merge_bytes;
-  static constexpr int bytes = prefill_bytes > decode_bytes ? prefill_bytes : decode_bytes;
+  static constexpr int prefill_bytes = (kKinds & 1) ? 2 * kKeysPerStage * (kStride + vStride) : 0;
+  static constexpr int decode_v_bytes = NW * 2 * (2 * kPage * D * 2);   // per-wave double buffer
+  static constexpr int merge_bytes = NW * 8 * D * 4 + 2 * NW * 8 * 4;
+  // decode-only kernels keep their V buffers in separate arrays; the mixed kernel carves them here
+  static constexpr int decode_bytes = (kKinds == 3) ? decode_v_bytes : 0;
+  static constexpr int bytes0 = prefill_bytes > decode_bytes ? prefill_bytes : decode_bytes;
+  static constexpr int bytes = bytes0 > 16 ? bytes0 : 16;
 };
 
 // ------------------------------------------------------------------------------------------------
@@ -222,7 +225,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 // ------------------------------------------------------------------------------------------------
 template <int D>
 __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile, int g, char* smem) {
-  constexpr int KS = Lds<D>::kStride, VS = Lds<D>::vStride;
+  constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
   constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
   constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
   constexpr int CPR = D / 8;                        // 16-byte chunks per K/V row
@@ -437,15 +440,10 @@ __device__ __forceinline__ void lds_dma16(const void* g, char* lds_base) {
 }
 
 template <int D>
-__device__ __forceinline__ void decode_issue(const AttnArgs& a, const int* s_pages, int p_begin, int p_end,
-                                             int g, int kv, int pi, DecodeK<D>& K, char* vdst) {
+__device__ __forceinline__ void decode_issue(const AttnArgs& a, int phys_a, int phys_b, bool pb_ok, int pa,
+                                             int g, int kv, DecodeK<D>& K, char* vdst) {
   using VT = VTile<D>;
   const int lane = threadIdx.x & 63, gi = lane >> 4, hh = lane & 15;
-  const int pa = p_begin + 2 * pi;
-  const bool pb_ok = pa + 1 < p_end;
-  const int pb = pb_ok ? pa + 1 : pa;               // a missing second page re-reads the first
-  const int phys_a = s_pages[pa - p_begin];
-  const int phys_b = s_pages[pb - p_begin];
   const size_t head_stride = (size_t)kPage * D;
   const size_t ga = ((size_t)phys_a * a.num_kv_heads + g) * head_stride;
   const size_t gb = ((size_t)phys_b * a.num_kv_heads + g) * head_stride;
@@ -525,13 +523,50 @@ __device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<
 // vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
 #define PEARL_VMCNT(n) (((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
 
+// Page ids of the pair a wave will issue next, read with scalar loads from the block table.
+struct PairPages {
+  int phys_a, phys_b, pa;
+  bool pb_ok;
+};
+
+// The block table is read-only for the whole kernel; reading it through the constant address
+// space lets the compiler use scalar loads (counted by lgkmcnt, not vmcnt) for these uniform reads.
+typedef const __attribute__((address_space(4))) int32_t* ConstI32Ptr;
+
+__device__ __forceinline__ PairPages pair_pages(ConstI32Ptr bt_row, int p_begin, int p_end, int pi, int num_pages) {
+  PairPages pp;
+  pp.pa = p_begin + 2 * pi;
+  pp.pb_ok = pp.pa + 1 < p_end;
+  pp.phys_a = clamp_page(bt_row[pp.pa], num_pages);
+  // a missing second page re-reads the first (index stays inside the row)
+  pp.phys_b = pp.pb_ok ? clamp_page(bt_row[pp.pa + 1], num_pages) : pp.phys_a;
+  return pp;
+}
+
+// One pipeline step: issue the next pair (K into k_next, V by DMA into v_next), then consume the
+// current pair from k_cur / v_cur.  The step is branch-free: a wave with no further pair re-issues
+// its current pair (L2 hits, results unused), so every step leaves exactly one pair in flight.
+// The two V buffers are __restrict__ parameters of this one function, so the compiler knows the
+// reads of v_cur cannot alias the DMA still writing v_next and waits only for the current pair.
 template <int D>
-__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, char* smem, int* s_pages) {
+__device__ __forceinline__ void decode_step(const AttnArgs& a, const PairPages& cur, const PairPages& nxt, int g,
+                                            int kv, DecodeK<D>& k_next, const DecodeK<D>& k_cur,
+                                            char* __restrict__ v_next, const char* __restrict__ v_cur,
+                                            const bf16x8* qop, f32x4* oacc, float& m_run, float& l_run) {
+  constexpr int PAIR_LOADS = 2 * DecodeK<D>::KB + VTile<D>::NDMA;   // vector-memory ops per pair
+  decode_issue<D>(a, nxt.phys_a, nxt.phys_b, nxt.pb_ok, nxt.pa, g, kv, k_next, v_next);
+  __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));              // the current pair has landed
+  decode_consume<D>(a, k_cur, cur.pa, cur.pb_ok, kv, qop, oacc, m_run, l_run, v_cur);
+}
+
+template <int D, int NW>
+__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, char* vbufA, char* vbufB) {
+  constexpr int NT = NW * 64;
   using VT = VTile<D>;
   constexpr int MB = D / 16;
   constexpr int KB = DecodeK<D>::KB;
   constexpr int PAIR_LOADS = 2 * KB + VT::NDMA;    // vector-memory instructions issued per pair
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
   const int gi = lane >> 4, hh = lane & 15;
   const SeqInfo si = a.seqinfo[b];
   const int G = a.group, H_q = a.num_q_heads;
@@ -541,13 +576,10 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
   const int p_end = min(p_begin + a.pages_per_split, n_pages);
   const int n_pairs = (p_end - p_begin + 1) / 2;
   const bool head_ok = hh < G;
-  char* vb0 = smem + w * 2 * VT::PAIR_BYTES;
-  char* vb1 = vb0 + VT::PAIR_BYTES;
+  char* vb0 = vbufA + w * VT::PAIR_BYTES;
+  char* vb1 = vbufB + w * VT::PAIR_BYTES;
 
-  // stage this split's physical page ids once (clamped into the pool)
-  const int32_t* bt_row = a.block_table + (size_t)b * a.bt_stride;
-  for (int i = threadIdx.x; i < p_end - p_begin; i += kThreads) s_pages[i] = clamp_page(bt_row[p_begin + i], a.num_pages);
-  __syncthreads();
+  const ConstI32Ptr bt_row = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
 
   bf16x8 qop[KB];
   {
@@ -559,41 +591,37 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
     }
   }
   DecodeK<D> kA, kB;
-  if (w < n_pairs) decode_issue<D>(a, s_pages, p_begin, p_end, g, kv, w, kA, vb0);
+  const int last = n_pairs - 1;
+  PairPages cur = pair_pages(bt_row, p_begin, p_end, min(w, last), a.num_pages);
+  if (w < n_pairs) decode_issue<D>(a, cur.phys_a, cur.phys_b, cur.pb_ok, cur.pa, g, kv, kA, vb0);
   f32x4 oacc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) oacc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  for (int pi = w; pi < n_pairs; pi += 2 * kWaves) {
-    // the next pair's loads go out before this pair is consumed
-    const int pj = pi + kWaves;
-    if (pj < n_pairs) {
-      decode_issue<D>(a, s_pages, p_begin, p_end, g, kv, pj, kB, vb1);
-      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));   // this pair's K and V have landed
-    } else {
-      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
-    }
-    decode_consume<D>(a, kA, p_begin + 2 * pi, p_begin + 2 * pi + 1 < p_end, kv, qop, oacc, m_run, l_run, vb0);
+  // page ids run one pair ahead of the loads, which run one pair ahead of the compute
+  PairPages nxt = w + NW < n_pairs ? pair_pages(bt_row, p_begin, p_end, w + NW, a.num_pages) : cur;
+  for (int pi = w; pi < n_pairs; pi += 2 * NW) {
+    const int pj = pi + NW, pk = pj + NW;
+    const PairPages n2 = pk < n_pairs ? pair_pages(bt_row, p_begin, p_end, pk, a.num_pages) : nxt;
+    decode_step<D>(a, cur, nxt, g, kv, kB, kA, vb1, vb0, qop, oacc, m_run, l_run);
     if (pj >= n_pairs) break;
-    const int pk = pj + kWaves;
-    if (pk < n_pairs) {
-      decode_issue<D>(a, s_pages, p_begin, p_end, g, kv, pk, kA, vb0);
-      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));
-    } else {
-      __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
-    }
-    decode_consume<D>(a, kB, p_begin + 2 * pj, p_begin + 2 * pj + 1 < p_end, kv, qop, oacc, m_run, l_run, vb1);
+    const PairPages n3 = pk + NW < n_pairs ? pair_pages(bt_row, p_begin, p_end, pk + NW, a.num_pages) : n2;
+    decode_step<D>(a, nxt, n2, g, kv, kA, kB, vb0, vb1, qop, oacc, m_run, l_run);
+    cur = n2;
+    nxt = n3;
   }
+  __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));      // drain the trailing re-issued pair
   // each head's four lane groups hold different keys: sum their l
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
 
-  // merge the 8 waves' states through LDS (reuses the V buffers)
+  // merge the waves' states through LDS
   __syncthreads();
-  float* mo = reinterpret_cast<float*>(smem);                 // [wave][8 heads][D]
-  float* mm = mo + kWaves * 8 * D;                            // [wave][8]
-  float* ml = mm + kWaves * 8;                                // [wave][8]
+  static_assert(Lds<D, NW, 2>::merge_bytes <= NW * VT::PAIR_BYTES, "merge scratch fits in a V buffer");
+  float* mo = reinterpret_cast<float*>(vbufA);                // [wave][8 heads][D]
+  float* mm = mo + NW * 8 * D;                            // [wave][8]
+  float* ml = mm + NW * 8;                                // [wave][8]
   if (head_ok) {
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
@@ -602,14 +630,14 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
   }
   __syncthreads();
   const int n_splits = si.kind >> 4;
-  for (int t = threadIdx.x; t < G * D; t += kThreads) {
+  for (int t = threadIdx.x; t < G * D; t += NT) {
     const int head = t / D, dim = t - head * D;
     float M = -INFINITY;
 #pragma unroll
-    for (int ww = 0; ww < kWaves; ++ww) M = fmaxf(M, mm[ww * 8 + head]);
+    for (int ww = 0; ww < NW; ++ww) M = fmaxf(M, mm[ww * 8 + head]);
     float L = 0.f, o = 0.f;
 #pragma unroll
-    for (int ww = 0; ww < kWaves; ++ww) {
+    for (int ww = 0; ww < NW; ++ww) {
       const float f = fexp2(mm[ww * 8 + head] - M);
       L += f * ml[ww * 8 + head];
       o += f * mo[(ww * 8 + head) * D + dim];
@@ -633,10 +661,21 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
 // come first (largest work), decode splits fill the tail.
 // ------------------------------------------------------------------------------------------------
 // kKinds: 1 = prefill tiles only, 2 = decode splits only, 3 = both (mixed batches).
+template <int D, int kKinds> struct KernelCfg {
+  static constexpr int NW = kWaves;
+  static constexpr int NT = NW * 64;
+};
+
 template <int D, int kKinds>
-__global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a, int max_pre) {
-  __shared__ __attribute__((aligned(16))) char smem[Lds<D>::bytes];
-  __shared__ int s_pages[kMaxPagesPerSplit];
+__global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnArgs a, int max_pre) {
+  constexpr int NW = KernelCfg<D, kKinds>::NW;
+  __shared__ __attribute__((aligned(16))) char smem[Lds<D, NW, kKinds>::bytes];
+  // the two V buffers of the decode pipeline are separate objects so the LDS reads of one are
+  // known not to alias the LDS-DMA writes still in flight into the other
+  __shared__ __attribute__((aligned(16))) char vbufA_[(kKinds == 2) ? NW * VTile<D>::PAIR_BYTES : 16];
+  __shared__ __attribute__((aligned(16))) char vbufB_[(kKinds == 2) ? NW * VTile<D>::PAIR_BYTES : 16];
+  char* vbufA = (kKinds == 2) ? vbufA_ : smem;
+  char* vbufB = (kKinds == 2) ? vbufB_ : smem + NW * VTile<D>::PAIR_BYTES;
   __shared__ int s_item[2];
   const int n_items = a.ws_hdr[kHdrNumItems];
   const int n_pre = a.ws_hdr[kHdrNumPre];
@@ -651,13 +690,14 @@ __global__ __launch_bounds__(kThreads) void attn_kernel(AttnArgs a, int max_pre)
     const int g = item - e * H_kv;
     if (e < n_pre) {
       if constexpr ((kKinds & 1) != 0) {
+        static_assert(NW == kWaves, "prefill tiles use 8 waves");
         const int2 en = a.entries[e];
         prefill_tile<D>(a, en.x, en.y, g, smem);
       }
     } else {
       if constexpr ((kKinds & 2) != 0) {
         const int2 en = a.entries[max_pre + (e - n_pre)];
-        decode_split<D>(a, en.x, en.y, g, smem, s_pages);
+        decode_split<D, NW>(a, en.x, en.y, g, vbufA, vbufB);
       }
     }
     __syncthreads();
@@ -718,7 +758,7 @@ struct DevCache {
 template <int D, int K>
 int occupancy_of() {
   int o = 1;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, attn_kernel<D, K>, kThreads, 0) != hipSuccess || o < 1) o = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, attn_kernel<D, K>, KernelCfg<D, K>::NT, 0) != hipSuccess || o < 1) o = 1;
   return o;
 }
 DevCache g_cache[64];
@@ -772,15 +812,15 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t 
   const int occ = c.occ[head_dim == 128 ? 1 : 0][kinds];
   int64_t grid = (int64_t)c.num_cu * occ;
   if (grid > max_items) grid = max_items;
-  const dim3 g((unsigned)grid), blk(kThreads);
+  const dim3 g((unsigned)grid);
   if (head_dim == 64) {
-    if (kinds == 1) hipLaunchKernelGGL((attn_kernel<64, 1>), g, blk, 0, stream, a, max_pre);
-    else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<64, 2>), g, blk, 0, stream, a, max_pre);
-    else hipLaunchKernelGGL((attn_kernel<64, 3>), g, blk, 0, stream, a, max_pre);
+    if (kinds == 1) hipLaunchKernelGGL((attn_kernel<64, 1>), g, dim3(KernelCfg<64, 1>::NT), 0, stream, a, max_pre);
+    else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<64, 2>), g, dim3(KernelCfg<64, 2>::NT), 0, stream, a, max_pre);
+    else hipLaunchKernelGGL((attn_kernel<64, 3>), g, dim3(KernelCfg<64, 3>::NT), 0, stream, a, max_pre);
   } else {
-    if (kinds == 1) hipLaunchKernelGGL((attn_kernel<128, 1>), g, blk, 0, stream, a, max_pre);
-    else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<128, 2>), g, blk, 0, stream, a, max_pre);
-    else hipLaunchKernelGGL((attn_kernel<128, 3>), g, blk, 0, stream, a, max_pre);
+    if (kinds == 1) hipLaunchKernelGGL((attn_kernel<128, 1>), g, dim3(KernelCfg<128, 1>::NT), 0, stream, a, max_pre);
+    else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<128, 2>), g, dim3(KernelCfg<128, 2>::NT), 0, stream, a, max_pre);
+    else hipLaunchKernelGGL((attn_kernel<128, 3>), g, dim3(KernelCfg<128, 3>::NT), 0, stream, a, max_pre);
   }
   return hipGetLastError();
 }
