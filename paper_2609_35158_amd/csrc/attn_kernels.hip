@@ -63,6 +63,10 @@ __device__ __forceinline__ bf16x8 concat_tr(i16x4 a, i16x4 b) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// The block table is read-only for the whole kernel; reading it through the constant address
+// space lets the compiler use scalar loads (counted by lgkmcnt, not vmcnt) for these uniform reads.
+typedef const __attribute__((address_space(4))) int32_t* ConstI32Ptr;
+
 __device__ __forceinline__ int clamp_page(int p, int num_pages) {
   return p < 0 ? 0 : (p >= num_pages ? num_pages - 1 : p);
 }
@@ -71,7 +75,7 @@ __device__ __forceinline__ int clamp_page(int p, int num_pages) {
 // NW = waves per workgroup; kinds as in attn_kernel.
 template <int D, int NW, int kKinds> struct Lds {
   static constexpr int kStride = D * 2 + 16;
-  static constexpr int vStride = D * 2 + 32;
+  static constexpr int vStride = D * 2 + 64;   // 320 B at d=128: conflict-free transpose reads
   static constexpr int prefill_bytes = (kKinds & 1) ? 2 * kKeysPerStage * (kStride + vStride) : 0;
   static constexpr int decode_v_bytes = NW * 2 * (2 * kPage * D * 2);   // per-wave double buffer
   static constexpr int merge_bytes = NW * 8 * D * 4 + 2 * NW * 8 * 4;
@@ -234,7 +238,8 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
   char* kbuf0 = smem;
   char* vbuf0 = smem + 2 * kKeysPerStage * KS;
 
-  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6, half = lane >> 5;
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
   const SeqInfo si = a.seqinfo[b];
   const int G = a.group;
   const int t0 = tile * a.tokens_per_tile;
@@ -267,115 +272,133 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
   float m_run = -INFINITY, l_run = 0.f;
 
   const int n_steps = (kv_needed + kKeysPerStage - 1) / kKeysPerStage;
-  const int32_t* bt_row = a.block_table + (size_t)b * a.bt_stride;
 
-  u32x4 kreg[NCH], vreg[NCH];
-  auto load_stage = [&](int step) {
+  // K/V staging: chunk i of this thread is 16 bytes of key row kk = cidx / CPR of the stage; the
+  // stage's page index of that row is the same for the whole wave, so it comes from a scalar
+  // load of the block table.  Loads are unconditional (rows past the last needed key re-read a
+  // valid page and are zeroed when stored to LDS) and run two stages ahead of the compute.
+  const ConstI32Ptr bt_c = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
+  const int last_pidx = (kv_needed - 1) / kPage;
+  struct Stage { u32x4 k[NCH], v[NCH]; };
+  auto load_stage = [&](int step, Stage& S) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int cidx = threadIdx.x + i * kThreads;
       const int kk = cidx / CPR, dc = cidx - kk * CPR;
       const int j = step * kKeysPerStage + kk;
-      if (j < kv_needed) {
-        const int page = clamp_page(bt_row[j / kPage], a.num_pages);
-        const size_t off = ((size_t)page * H_kv + g) * head_stride + (size_t)(j % kPage) * D + dc * 8;
-        kreg[i] = ld16(a.k_pool + off);
-        vreg[i] = ld16(a.v_pool + off);
-      } else {
-        kreg[i] = u32x4{0u, 0u, 0u, 0u};
-        vreg[i] = u32x4{0u, 0u, 0u, 0u};
-      }
+      const int pidx = min(step * (kKeysPerStage / kPage) + (64 * w + kThreads * i) / (kPage * CPR), last_pidx);
+      const int page = clamp_page(bt_c[pidx], a.num_pages);
+      const size_t off = ((size_t)page * H_kv + g) * head_stride + (size_t)(j % kPage) * D + dc * 8;
+      S.k[i] = ld16(a.k_pool + off);
+      S.v[i] = ld16(a.v_pool + off);
     }
   };
-  auto store_stage = [&](int buf) {
+  auto store_stage = [&](int step, int buf, const Stage& S) {
     char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
     char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
+    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
       const int cidx = threadIdx.x + i * kThreads;
       const int kk = cidx / CPR, dc = cidx - kk * CPR;
-      *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = kreg[i];
-      *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = vreg[i];
+      const bool ok = step * kKeysPerStage + kk < kv_needed;
+      *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = ok ? S.k[i] : zero;
+      *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = ok ? S.v[i] : zero;
     }
   };
+  auto compute = [&](int step, int buf) {
+      const char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
+      const char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
+      const int k0 = step * kKeysPerStage;
 
-  load_stage(0);
-  store_stage(0);
-  __syncthreads();
-  for (int step = 0; step < n_steps; ++step) {
-    const int buf = step & 1;
-    if (step + 1 < n_steps) load_stage(step + 1);
-    const char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
-    const char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
-    const int k0 = step * kKeysPerStage;
-
-    // S^T = K Q^T for two 32-key sub-tiles
-    f32x16 s[2];
+      // S^T = K Q^T for two 32-key sub-tiles
+      f32x16 s[2];
 #pragma unroll
-    for (int st = 0; st < 2; ++st) {
+      for (int st = 0; st < 2; ++st) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
+        for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
 #pragma unroll
-      for (int kb = 0; kb < KB; ++kb) {
-        const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2);
-        s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], s[st], 0, 0, 0);
+        for (int kb = 0; kb < KB; ++kb) {
+          const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2);
+          s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], s[st], 0, 0, 0);
+        }
       }
-    }
-    // causal mask (only on steps that reach past some row's last visible key)
-    if (k0 + kKeysPerStage - 1 > wave_min_limit) {
+      // causal mask (only on steps that reach past some row's last visible key)
+      if (k0 + kKeysPerStage - 1 > wave_min_limit) {
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int key = k0 + 32 * st + (r & 3) + 8 * (r >> 2) + 4 * half;
+            if (key > row_limit) s[st][r] = -INFINITY;
+          }
+      }
+      // online softmax (base 2)
+      float mx = s[0][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      // the row maximum only moves when this tile exceeds it; the O rescale is skipped when no
+      // row of the wave moved (the largest weight of a row is then exactly 1 in bf16)
+      const bool grow = mx * c > m_run;
+      const float m_new = grow ? mx * c : m_run;
+      const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
+      float psum = 0.f;
+      bf16x8 pop[2][2];
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const int key = k0 + 32 * st + (r & 3) + 8 * (r >> 2) + 4 * half;
-          if (key > row_limit) s[st][r] = -INFINITY;
+          const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
+          psum += pv;
+          pop[st][r >> 3][r & 7] = (__bf16)pv;
         }
-    }
-    // online softmax (base 2)
-    float mx = s[0][0];
+      l_run = l_run * alpha + psum;
+      if (__ballot(grow)) {
 #pragma unroll
-    for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx * c);
-    const float alpha = fexp2(m_run - m_new);
-    float psum = 0.f;
-    bf16x8 pop[2][2];
-#pragma unroll
-    for (int st = 0; st < 2; ++st)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
-        psum += pv;
-        pop[st][r >> 3][r & 7] = (__bf16)pv;
+          for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
       }
-    l_run = l_run * alpha + psum;
-    if (__ballot(alpha != 1.0f)) {
+      m_run = m_new;
+      // O^T += V^T P^T
+      {
+        const int gi = lane >> 4, j = lane & 15;
+        const int krow = 4 * (gi >> 1) + (j >> 2);
+        const int dcol = 16 * (gi & 1) + 4 * (j & 3);
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
+        for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
-    }
-    m_run = m_new;
-    // O^T += V^T P^T
-    {
-      const int gi = lane >> 4, j = lane & 15;
-      const int krow = 4 * (gi >> 1) + (j >> 2);
-      const int dcol = 16 * (gi & 1) + 4 * (j & 3);
+          for (int st = 0; st < 2; ++st)
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            const int off = (32 * st + 16 * kk + krow) * VS + (32 * mb + dcol) * 2;
-            const i16x4 v0 = lds_read_tr(vb_, off);
-            const i16x4 v1 = lds_read_tr(vb_, off + 8 * VS);
-            oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(concat_tr(v0, v1), pop[st][kk], oacc[mb], 0, 0, 0);
-          }
-    }
-    if (step + 1 < n_steps) store_stage(buf ^ 1);
+            for (int kk = 0; kk < 2; ++kk) {
+              const int off = (32 * st + 16 * kk + krow) * VS + (32 * mb + dcol) * 2;
+              const i16x4 v0 = lds_read_tr(vb_, off);
+              const i16x4 v1 = lds_read_tr(vb_, off + 8 * VS);
+              oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(concat_tr(v0, v1), pop[st][kk], oacc[mb], 0, 0, 0);
+            }
+      }
+  };
+
+  Stage sA, sB;
+  const int last_step = n_steps - 1;
+  load_stage(0, sA);
+  load_stage(min(1, last_step), sB);
+  store_stage(0, 0, sA);
+  __syncthreads();
+  for (int step = 0; step < n_steps; step += 2) {
+    // even step: sB holds step+1 (in flight); refill sA with step+2 (past the end: a repeat)
+    load_stage(min(step + 2, last_step), sA);
+    compute(step, 0);
+    if (step + 1 < n_steps) store_stage(step + 1, 1, sB);
+    __syncthreads();
+    if (step + 1 >= n_steps) break;
+    // odd step: sA holds step+2; refill sB with step+3
+    load_stage(min(step + 3, last_step), sB);
+    compute(step + 1, 1);
+    if (step + 2 < n_steps) store_stage(step + 2, 0, sA);
     __syncthreads();
   }
 
@@ -491,8 +514,9 @@ __device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<
   float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])), fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(m_run, mx * c);
-  const float alpha = fexp2(m_run - m_new);
+  const bool grow = mx * c > m_run;   // as in prefill_tile
+  const float m_new = grow ? mx * c : m_run;
+  const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
   bf16x8 pop;
   float psum = 0.f;
 #pragma unroll
@@ -504,8 +528,10 @@ __device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<
     pop[4 + r] = (__bf16)p1;
   }
   l_run = l_run * alpha + psum;
+  if (__ballot(grow)) {
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb) oacc[mb] *= alpha;
+    for (int mb = 0; mb < MB; ++mb) oacc[mb] *= alpha;
+  }
   m_run = m_new;
   {
     const int j = lane & 15;
@@ -529,9 +555,6 @@ struct PairPages {
   bool pb_ok;
 };
 
-// The block table is read-only for the whole kernel; reading it through the constant address
-// space lets the compiler use scalar loads (counted by lgkmcnt, not vmcnt) for these uniform reads.
-typedef const __attribute__((address_space(4))) int32_t* ConstI32Ptr;
 
 __device__ __forceinline__ PairPages pair_pages(ConstI32Ptr bt_row, int p_begin, int p_end, int pi, int num_pages) {
   PairPages pp;

@@ -102,14 +102,29 @@ def oracle_sampled(case: workloads.Case, seqs: Sequence[int], tokens: Optional[D
     return out_o, out_l
 
 
+def bf16_ulp(x: np.ndarray) -> np.ndarray:
+    """Spacing of bf16 numbers at |x| (8 significant bits)."""
+    e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -126)))
+    return 2.0 ** (e - 7)
+
+
 def assert_close(gpu_o_bits: np.ndarray, ref_o: np.ndarray, gpu_lse: Optional[np.ndarray] = None,
-                 ref_lse: Optional[np.ndarray] = None, what: str = "") -> dict:
+                 ref_lse: Optional[np.ndarray] = None, what: str = "", ulp_slack: float = 0.0) -> dict:
+    """Outputs within max-abs 1e-2 and mean-abs 1e-3 of the float64 oracle.  With ulp_slack > 0
+    (stress inputs whose outputs reach |o| >= 4, where rounding to bf16 alone moves a value by up
+    to 2^-9 |o| > 1e-2), each element may also deviate by ulp_slack bf16 ulps of the reference."""
     st = oracle.compare(gpu_o_bits, ref_o)
     say("   parity %s: n=%d max_abs=%.3e mean_abs=%.3e max_ulp=%.1f" % (what, st["n"], st["max_abs"],
                                                                           st["mean_abs"], st["max_ulp"]))
     assert st["n"] > 0, "nothing compared"
     assert st["nonfinite_gpu"] == 0, "non-finite GPU outputs (%s)" % what
-    assert st["max_abs"] <= MAX_ABS, "max_abs %.3e > %.1e (%s)" % (st["max_abs"], MAX_ABS, what)
+    if ulp_slack > 0:
+        g = oracle.bf16_bits_to_f64(gpu_o_bits)
+        m = np.isfinite(ref_o)
+        excess = np.abs(g[m] - ref_o[m]) - (MAX_ABS + ulp_slack * bf16_ulp(ref_o[m]))
+        assert excess.max() <= 0, "max excess over 1e-2 + %g ulp: %.3e (%s)" % (ulp_slack, excess.max(), what)
+    else:
+        assert st["max_abs"] <= MAX_ABS, "max_abs %.3e > %.1e (%s)" % (st["max_abs"], MAX_ABS, what)
     assert st["mean_abs"] <= MEAN_ABS, "mean_abs %.3e > %.1e (%s)" % (st["mean_abs"], MEAN_ABS, what)
     if gpu_lse is not None and ref_lse is not None:
         m = np.isfinite(ref_lse)

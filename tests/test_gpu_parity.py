@@ -261,3 +261,56 @@ def test_device_length_violation_reports_and_writes_nothing():
     torch.cuda.synchronize()
     assert torch.all(out2 == 7.0)
     assert not torch.all(out == 7.0)
+
+
+@pytest.mark.parametrize("pattern", ["ramp", "ramp_down", "large"])
+def test_score_range_and_running_max(pattern):
+    """Scores that grow (or shrink) steadily along the context make the running maximum move on
+    every tile; large-magnitude q/k give scores far outside exp's fp32 range without the max
+    subtraction.  All modes must still match the oracle."""
+    say("case: score pattern %s" % pattern)
+    ctx = np.array([1500, 700, 3000]); ql = np.array([90, 1, 1])
+    case = workloads.build_case("range", 21, 32, 4, 128, ctx, ql, device="cuda")
+    gen = torch.Generator(device="cuda").manual_seed(5)
+    if pattern in ("ramp", "ramp_down"):
+        sign = 1.0 if pattern == "ramp" else -1.0
+        # q . k_j grows linearly with the key position j through the first coordinate
+        bt = case.block_table.cpu().numpy()
+        kp = case.k_pool.float()
+        for b in range(3):
+            n = int(ctx[b])
+            pos = torch.arange(n, dtype=torch.float32, device="cuda")
+            pages = torch.from_numpy(bt[b][np.arange(n) // 16].astype(np.int64)).cuda()
+            slots = torch.from_numpy((np.arange(n) % 16).astype(np.int64)).cuda()
+            kp[pages, :, slots, 0] = (sign * pos * 0.03)[:, None]
+        case.k_pool = kp.to(torch.bfloat16)
+        qf = case.q.float()
+        qf[..., 0] = 8.0
+        case.q = qf.to(torch.bfloat16).contiguous()
+        kn = case.k_new.float()
+        kn[..., 0] = sign * (torch.from_numpy(np.concatenate([np.arange(c, c + n) for c, n in zip(ctx, ql)]))
+                             .float().cuda()[:, None] * 0.03)
+        case.k_new = kn.to(torch.bfloat16).contiguous()
+    else:
+        case.q = (case.q.float() * 6.0).to(torch.bfloat16).contiguous()
+        case.k_pool = (case.k_pool.float() * 4.0).to(torch.bfloat16)
+        case.k_new = (case.k_new.float() * 4.0).to(torch.bfloat16).contiguous()
+    kr, vr = _append_and_check(case)
+    o_ref, l_ref = oracle_full(case, kr, vr)
+    for mode in ("prefill", "mixed"):
+        out, lse = gpu_attend(case, mode)
+        torch.cuda.synchronize()
+        assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="%s %s" % (pattern, mode),
+                     ulp_slack=2.0 if pattern == "large" else 0.0)
+    dec = [1, 2]
+    sub = workloads.Case(name="sub", seed=0, num_q_heads=32, num_kv_heads=4, head_dim=128,
+                         ctx_lens=case.ctx_lens[dec], q_lens=case.q_lens[dec],
+                         block_table=case.block_table[dec].contiguous(), k_pool=case.k_pool,
+                         v_pool=case.v_pool, k_new=None, v_new=None,
+                         q=case.q[torch.tensor([int(case.cu_q_lens[b]) for b in dec]).cuda()].contiguous(),
+                         scale=case.scale)
+    out_d, lse_d = gpu_attend(sub, "decode")
+    torch.cuda.synchronize()
+    rows = [int(case.cu_q_lens[b]) for b in dec]
+    assert_close(bits(out_d), o_ref[rows], lse_d.cpu().numpy(), l_ref[rows], what="%s decode" % pattern,
+                 ulp_slack=2.0 if pattern == "large" else 0.0)
