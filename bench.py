@@ -327,7 +327,7 @@ def main():
         },
         "hbm_tbps_step": round(nbytes / (ms_step * 1e-3) / 1e12, 4),
         "roofline": {
-            "kernel": "attn_kernel<128> (decode split items)",
+            "kernel": "attn_kernel<128, decode> (decode split items)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": measured_traffic("attn_kernel<128>", "qwen3-8b-decode-b64"),

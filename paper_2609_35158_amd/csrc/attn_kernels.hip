@@ -313,14 +313,13 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
 
       // S^T = K Q^T for two 32-key sub-tiles
       f32x16 s[2];
+      const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
-        for (int r = 0; r < 16; ++r) s[st][r] = 0.f;
-#pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
           const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2);
-          s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], s[st], 0, 0, 0);
+          s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
         }
       }
       // causal mask (only on steps that reach past some row's last visible key)
