@@ -12,7 +12,8 @@ The same line carries:
                 events around each launch inside the timed region;
   cpu_baseline  the CPU oracle (numpy float64) timed on this host on a bounded sample;
   secondary     prefill-append TFLOP/s (Qwen3-8B shape), Qwen3-30B-A3B-shaped decode at batch
-                256/128/32, the colocated mixed batch, and kv_append GB/s.
+                256/128/32, the colocated mixed batch, kv_append GB/s, and a decode/prefill
+                interference sweep (one mixed launch vs decode alone as prefill chunks grow).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-secondary] [--no-cpu]
 """
@@ -177,6 +178,81 @@ def time_append(torch, pa, step, steps):
         step(lambda: None, attention=False)
         pa.load().pearl_set_kernel_events(None, None)
     return run_timed(torch, pa, one, steps, 1)
+
+
+# ------------------------------------------------------------------------------------------------
+# decode/prefill interference at kernel level
+# ------------------------------------------------------------------------------------------------
+
+PD_CHUNKS = (1, 2, 4, 8, 16)
+PD_SIZES = (256, 512, 1024, 2048)
+
+
+def pd_interference(torch, pa, workloads, steps, warmup):
+    """Cost of colocating prefill with decode inside one launch (the kernel-level analogue of the
+    paper's observation that prefill insertions stall the decode batch; Motivation, PD
+    interference figure).  A fixed Qwen3-30B-A3B-shaped decode batch -- 192 sequences, contexts
+    uniform in [2048, 32768] -- runs alone, then in one mixed launch with k prefill chunks of s new
+    tokens on 8192-token contexts; the chunks also run alone.  All points share one pool."""
+    import numpy as np
+    kmax, smax = max(PD_CHUNKS), max(PD_SIZES)
+    base = workloads.mixed_colocated("cuda", n_prefill=kmax, chunk=smax)
+    fill, _ = make_step(torch, pa, base, "mixed")
+    fill(lambda: None, attention=False)           # write every position any sub-batch reads
+    torch.cuda.synchronize()
+    dec_seqs = list(range(kmax, base.batch))
+    ndec = len(dec_seqs)
+
+    def time_attn(case, mode):
+        st, out = make_step(torch, pa, case, mode)
+        _, ms_k = run_timed(torch, pa, lambda hook: st(hook, append=False), steps, warmup)
+        del st, out
+        return ms_k
+
+    dec = workloads.sub_batch(base, dec_seqs)
+    t_dec = time_attn(dec, "decode")
+    t_dec_mixed = time_attn(dec, "mixed")
+    dec_bytes = attn_bytes(dec)
+    points = []
+    for s in PD_SIZES:
+        for k in PD_CHUNKS:
+            pre = workloads.sub_batch(base, list(range(k)), [s] * k)
+            mix = workloads.sub_batch(base, list(range(k)) + dec_seqs, [s] * k + [1] * ndec)
+            t_pre = time_attn(pre, "prefill")
+            t_mix = time_attn(mix, "mixed")
+            f_pre = attn_flops(pre)
+            points.append({
+                "chunks": k, "chunk_tokens": s, "prefill_tokens": k * s,
+                "prefill_tflop": round(f_pre / 1e12, 4),
+                "mixed_ms": round(t_mix, 4), "prefill_alone_ms": round(t_pre, 4),
+                "serial_ms": round(t_pre + t_dec, 4),
+                "decode_tok_s_in_mixed": round(ndec / (t_mix * 1e-3), 1),
+                "decode_slowdown": round(t_mix / t_dec, 4),
+                "overlap_saved_frac": round((t_pre + t_dec - t_mix) / (t_pre + t_dec), 4),
+                "prefill_tflops_alone": round(f_pre / (t_pre * 1e-3) / 1e12, 1),
+            })
+            log("bench:   pd k=%2d s=%4d: mixed %.3f ms, prefill alone %.3f, decode alone %.3f -> "
+                "decode slowdown %.2fx, %.1f%% saved vs serial"
+                % (k, s, t_mix, t_pre, t_dec, t_mix / t_dec, 100 * points[-1]["overlap_saved_frac"]))
+            del pre, mix
+    # least-squares line: mixed time = decode-alone time + TFLOP of prefill / rate
+    x = np.array([p["prefill_tflop"] for p in points])
+    y = np.array([p["mixed_ms"] for p in points]) - t_dec
+    slope = float((x * y).sum() / (x * x).sum())
+    entry = {
+        "workload": "pd-interference", "mode": "mixed",
+        "decode_batch": ndec, "decode_alone_ms": round(t_dec, 4),
+        "decode_alone_via_mixed_ms": round(t_dec_mixed, 4),
+        "decode_alone_GBps": round(dec_bytes / (t_dec * 1e-3) / 1e9, 1),
+        "decode_tok_s_alone": round(ndec / (t_dec * 1e-3), 1),
+        "prefill_ctx": int(base.ctx_lens[0]),
+        "added_ms_per_prefill_tflop": round(slope, 4),
+        "prefill_tflops_inside_mixed": round(1e3 / slope, 1) if slope > 0 else None,
+        "points": points,
+    }
+    del base, fill, dec
+    torch.cuda.empty_cache()
+    return entry
 
 
 # ------------------------------------------------------------------------------------------------
@@ -393,6 +469,9 @@ def main():
             sec.append(entry)
             del c, st, o
             torch.cuda.empty_cache()
+        if not only or "pd-interference" in only:
+            log("bench: secondary pd-interference")
+            sec.append(pd_interference(torch, pa, workloads, max(5, args.steps // 2), args.warmup))
         result["secondary"] = sec
     print(json.dumps(result), flush=True)
 

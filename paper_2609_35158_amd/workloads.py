@@ -253,6 +253,28 @@ def mixed_colocated(device="cpu", seed=5, n_prefill=8, chunk=512, prefill_ctx=81
     return case
 
 
+def sub_batch(case: Case, seqs, q_lens=None, name: Optional[str] = None) -> Case:
+    """A batch made of some sequences of ``case``, sharing its pools: sequence ``seqs[i]`` keeps its
+    cached context and block-table row and takes the first ``q_lens[i]`` of its new tokens (all of
+    them when ``q_lens`` is None).  Used to sweep batch composition over one generated pool."""
+    dev = case.q.device
+    seqs = np.asarray(seqs, dtype=np.int64)
+    full = case.q_lens[seqs].astype(np.int64)
+    ql = full if q_lens is None else np.asarray(q_lens, dtype=np.int64)
+    assert ql.shape == full.shape and np.all(ql >= 0) and np.all(ql <= full)
+    cu = case.cu_q_lens
+    parts = [np.arange(cu[b], cu[b] + n) for b, n in zip(seqs, ql)]
+    rows = torch.from_numpy(np.concatenate(parts) if parts else np.zeros(0, np.int64)).to(dev)
+    return Case(name=name or case.name + "-sub", seed=case.seed, num_q_heads=case.num_q_heads,
+                num_kv_heads=case.num_kv_heads, head_dim=case.head_dim,
+                ctx_lens=case.ctx_lens[seqs].astype(np.int32), q_lens=ql.astype(np.int32),
+                block_table=case.block_table.index_select(0, torch.from_numpy(seqs).to(dev)).contiguous(),
+                k_pool=case.k_pool, v_pool=case.v_pool,
+                k_new=case.k_new.index_select(0, rows).contiguous(),
+                v_new=case.v_new.index_select(0, rows).contiguous(),
+                q=case.q.index_select(0, rows).contiguous(), scale=case.scale)
+
+
 def random_small(seed: int, device="cpu", batch=None, H_kv=None, G=None, d=None,
                  max_ctx=300, max_q=40, decode_only=False, allow_zero_q=False) -> Case:
     """Small random shapes for fuzzing: ragged contexts (including 0) and chunk lengths."""

@@ -110,3 +110,33 @@ def test_mixed_colocated_fullsize():
     for b in seqs:
         rows = [cu[b] + t for t in tokens[b]]
         assert_close(ob[rows], o_ref[b][tokens[b]], lb[rows], l_ref[b][tokens[b]], what="mixed seq %d" % b)
+
+
+def test_pd_interference_sweep_points():
+    """The interference sweep's extreme points: 16 chunks of 2048 tokens and 1 chunk of 256 tokens
+    on 8192-token contexts, batched with 192 decodes in one mixed launch, on sub-batches of one
+    shared pool (as the benchmark builds them)."""
+    say("case: pd-interference sweep points (16 x 2048 and 1 x 256 prefill + 192 decode)")
+    base = workloads.mixed_colocated("cuda", n_prefill=16, chunk=2048)
+    gpu_append(base)
+    dec = list(range(16, base.batch))
+    rng = np.random.default_rng(7)
+    for k, s in ((16, 2048), (1, 256)):
+        case = workloads.sub_batch(base, list(range(k)) + dec, [s] * k + [1] * len(dec))
+        out, lse = gpu_attend(case, "mixed")
+        torch.cuda.synchronize()
+        assert torch.isfinite(out.float()).all() and torch.isfinite(lse).all()
+        pre = sorted({0, k - 1})
+        dsel = k + np.array(_pick(case.ctx_lens[k:], 3, rng))
+        tokens = {b: sorted({0, s - 1, s // 2, 255, 256 % s}) for b in pre}
+        for b in dsel:
+            tokens[int(b)] = [0]
+        seqs = pre + [int(b) for b in dsel]
+        o_ref, l_ref = oracle_sampled(case, seqs, tokens)
+        cu = case.cu_q_lens
+        ob, lb = bits(out), lse.cpu().numpy()
+        for b in seqs:
+            rows = [cu[b] + t for t in tokens[b]]
+            assert_close(ob[rows], o_ref[b][tokens[b]], lb[rows], l_ref[b][tokens[b]],
+                         what="pd k=%d s=%d seq %d" % (k, s, b))
+        del case, out, lse
