@@ -88,6 +88,8 @@ pearl_status check_seqs(const pearl_seq_desc* q, bool need_q_lens) {
     return fail(PEARL_ERR_INVALID_ARG, "bt_stride (%d) pages cannot hold max_kv_len (%d) tokens", q->bt_stride, q->max_kv_len);
   if ((int64_t)q->batch * q->bt_stride > INT32_MAX)
     return fail(PEARL_ERR_INVALID_ARG, "block table too large");
+  if (q->max_q_len > kMaxQLen) return fail(PEARL_ERR_UNSUPPORTED, "max_q_len (%d) > %d", q->max_q_len, kMaxQLen);
+  if (q->max_kv_len > kMaxKvLen) return fail(PEARL_ERR_UNSUPPORTED, "max_kv_len (%d) > %d", q->max_kv_len, kMaxKvLen);
   return PEARL_OK;
 }
 
@@ -100,7 +102,8 @@ Plan make_plan(const pearl_kv_shape* s, const pearl_seq_desc* q, int mode) {
   Plan pl;
   const int G = s->num_q_heads / s->num_kv_heads;
   const int pps = choose_pages_per_split(q->batch, s->num_kv_heads, q->max_kv_len, kPlanComputeUnits);
-  pl.lay = workspace_layout(q->batch, q->total_q, q->max_kv_len, s->num_q_heads, s->num_kv_heads, s->head_dim, G, pps);
+  pl.lay = workspace_layout(q->batch, q->total_q, q->max_kv_len, s->num_q_heads, s->num_kv_heads, s->head_dim, G, pps,
+                            q->cu_q_lens != nullptr);
   PlanParams& p = pl.p;
   p.mode = mode;
   p.batch = q->batch;
@@ -114,6 +117,8 @@ Plan make_plan(const pearl_kv_shape* s, const pearl_seq_desc* q, int mode) {
   p.pages_per_split = pps;
   p.max_pre = pl.lay.max_pre;
   p.max_dec = pl.lay.max_dec;
+  p.pre_slots = mode == kModeDecode ? 0 : pl.lay.pre_slots;
+  p.pre_jobs_cap = mode == kModeDecode ? 0 : pl.lay.pre_jobs_cap;
   return pl;
 }
 
@@ -156,6 +161,9 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   a.entries = reinterpret_cast<const int2*>(w + pl.lay.entries);
   a.part_o = reinterpret_cast<float*>(w + pl.lay.part_o);
   a.part_ml = reinterpret_cast<float*>(w + pl.lay.part_ml);
+  a.pre_jobs = reinterpret_cast<const int4*>(w + pl.lay.pre_jobs);
+  a.part_pre_o = reinterpret_cast<float*>(w + pl.lay.part_pre_o);
+  a.part_pre_ml = reinterpret_cast<float*>(w + pl.lay.part_pre_ml);
   a.bt_stride = q->bt_stride;
   a.num_pages = s->num_pages;
   a.num_q_heads = s->num_q_heads;
@@ -175,6 +183,10 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   if (mode != kModePrefill && pl.lay.max_dec > 0) {
     e = launch_merge(a, s->head_dim, q->batch, hs);
     if (e != hipSuccess) return fail(PEARL_ERR_HIP, "merge launch: %s", hipGetErrorString(e));
+  }
+  if (pl.p.pre_jobs_cap > 0) {
+    e = launch_merge_prefill(a, s->head_dim, pl.p.pre_jobs_cap, hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "prefill merge launch: %s", hipGetErrorString(e));
   }
   if (debug_mode()) {
     e = hipStreamSynchronize(hs);
@@ -204,11 +216,18 @@ int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_
 }
 
 WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_heads, int num_kv_heads,
-                          int head_dim, int group, int pages_per_split) {
+                          int head_dim, int group, int pages_per_split, bool has_prefill) {
   WsLayout l;
   const int T = kRowsPerTile / group;
-  // prefill entries: sum_b ceil(n_b / T) <= total_q / T + batch, and <= total_q
-  l.max_pre = std::min<int64_t>(total_q, total_q / T + batch);
+  // prefill tiles: sum_b ceil(n_b / T) <= total_q / T + batch, and <= total_q
+  const int64_t tiles = std::min<int64_t>(total_q, total_q / T + batch);
+  // split prefill items: every tile splits into at most ceil(max_kv_len / kMinSplitKeys) ranges,
+  // and the planner keeps the split items of a launch within kMaxPreSplitItems
+  l.pre_slots = 0;
+  if (has_prefill && max_kv_len > kMinSplitKeys)
+    l.pre_slots = std::min<int64_t>(kMaxPreSplitItems, (int64_t)num_kv_heads * tiles * cdiv(max_kv_len, kMinSplitKeys));
+  l.pre_jobs_cap = l.pre_slots / num_kv_heads;
+  l.max_pre = std::max<int64_t>(tiles, l.pre_jobs_cap);
   // decode entries: every sequence holds at most ceil(max_kv_len / 16) pages
   const int64_t max_pages = cdiv(std::max(max_kv_len, 1), kPage);
   l.max_dec = (int64_t)batch * cdiv(max_pages, pages_per_split);
@@ -219,6 +238,9 @@ WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_head
   l.entries = off; off = align256(off + sizeof(int2) * (size_t)(l.max_pre + l.max_dec));
   l.part_o = off; off = align256(off + sizeof(float) * (size_t)l.max_dec * num_q_heads * head_dim);
   l.part_ml = off; off = align256(off + sizeof(float) * 2 * (size_t)l.max_dec * num_q_heads);
+  l.pre_jobs = off; off = align256(off + sizeof(int4) * (size_t)l.pre_jobs_cap);
+  l.part_pre_o = off; off = align256(off + sizeof(float) * (size_t)l.pre_slots * kRowsPerTile * head_dim);
+  l.part_pre_ml = off; off = align256(off + sizeof(float) * 2 * (size_t)l.pre_slots * kRowsPerTile);
   l.total = off;
   (void)num_kv_heads;
   return l;
@@ -286,7 +308,7 @@ size_t pearl_attn_workspace_bytes(const pearl_kv_shape* shape, const pearl_seq_d
     const int G = shape->num_q_heads / shape->num_kv_heads;
     const int pps = choose_pages_per_split(seqs->batch, shape->num_kv_heads, seqs->max_kv_len, kPlanComputeUnits);
     return workspace_layout(seqs->batch, seqs->total_q, seqs->max_kv_len, shape->num_q_heads, shape->num_kv_heads,
-                            shape->head_dim, G, pps).total;
+                            shape->head_dim, G, pps, seqs->cu_q_lens != nullptr).total;
   } catch (...) {
     set_err("unexpected exception in pearl_attn_workspace_bytes");
     return 0;

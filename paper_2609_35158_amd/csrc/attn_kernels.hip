@@ -125,45 +125,98 @@ __global__ __launch_bounds__(256) void kv_append_kernel(
 // Planner: one workgroup validates the device-resident lengths against the host bounds and
 // builds the work list (prefill q-tiles, then decode page-range splits), so no host sync is
 // needed.  Writes the header, per-sequence records and entries; zeroes the work counter.
+//
+// Prefill tiles are split along the keys when the launch holds at most one tile item per compute
+// unit and its longest tile would outlast the average work per unit.  Work is estimated in
+// key-units: a prefill tile key (256 q-rows on MFMA) costs about 3/2 of a decode key (one K/V row
+// read from HBM).  A split covers kKeysPerStage-aligned key ranges [s S, (s+1) S) of the tile,
+// the last one running to the tile's end; splits start at or before the first key that only
+// some rows of the tile see (key ctx + t0 + 1), so every row sees at least one key of every
+// split.  S is at least kMinSplitKeys and at least the tile keys per unit, which keeps the split
+// items of a launch under 2 * kPlanComputeUnits (the partial-slot capacity).
 // ------------------------------------------------------------------------------------------------
 constexpr int kPlanThreads = 1024;
+
+__device__ __forceinline__ int tile_splits(int ctx, int t0, int split_keys) {
+  return split_keys > 0 ? (ctx + t0 + split_keys) / split_keys : 1;   // ceil((ctx + t0 + 1) / S)
+}
 
 __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     PlanParams p, const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ cu,
     int32_t* __restrict__ hdr, SeqInfo* __restrict__ seqinfo, int32_t* __restrict__ split_base,
-    int2* __restrict__ entries) {
-  __shared__ int s_err;
-  __shared__ long long s_scan[kPlanThreads];
-  __shared__ long long s_carry;
+    int2* __restrict__ entries, int4* __restrict__ pre_jobs) {
+  __shared__ int s_err, s_tiles, s_max_full, s_split_keys;
+  __shared__ unsigned long long s_pre_keys, s_dec_keys;
+  __shared__ int s_scan[3][kPlanThreads];
+  __shared__ int s_carry[3];
   const int tid = threadIdx.x;
-  if (tid == 0) { s_err = 0; s_carry = 0; }
+  const int T = p.tokens_per_tile;
+  if (tid == 0) {
+    s_err = 0; s_tiles = 0; s_max_full = 0; s_pre_keys = 0; s_dec_keys = 0;
+    s_carry[0] = s_carry[1] = s_carry[2] = 0;
+  }
   if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
   __syncthreads();
-  // pass 1: validate every sequence
-  for (int b = tid; b < p.batch; b += kPlanThreads) {
-    const int q_start = cu ? cu[b] : b;
-    const int q_len = cu ? cu[b + 1] - q_start : 1;
-    const int ctx = ctx_lens[b];
-    const long long kv = (long long)ctx + q_len;
-    bool bad = q_len < 0 || ctx < 0 || q_start < 0 || q_len > p.max_q_len ||
-               (long long)q_start + q_len > p.total_q || kv > p.max_kv_len ||
-               (kv + kPage - 1) / kPage > p.bt_stride;
-    if (p.mode == kModeDecode && q_len != 1) bad = true;
-    if (bad) atomicOr(&s_err, 1);
+  // pass 1: validate every sequence and total the work
+  {
+    int tiles = 0, max_full = 0;
+    unsigned long long pre_keys = 0, dec_keys = 0;
+    for (int b = tid; b < p.batch; b += kPlanThreads) {
+      const int q_start = cu ? cu[b] : b;
+      const int q_len = cu ? cu[b + 1] - q_start : 1;
+      const int ctx = ctx_lens[b];
+      const long long kv = (long long)ctx + q_len;
+      bool bad = q_len < 0 || ctx < 0 || q_start < 0 || q_len > p.max_q_len ||
+                 (long long)q_start + q_len > p.total_q || kv > p.max_kv_len ||
+                 (kv + kPage - 1) / kPage > p.bt_stride;
+      if (p.mode == kModeDecode && q_len != 1) bad = true;
+      if (bad) { atomicOr(&s_err, 1); continue; }
+      if (q_len <= 0) continue;
+      if (p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1)) {
+        dec_keys += (unsigned long long)kv;
+      } else {
+        const int nt = (q_len + T - 1) / T;
+        tiles += nt;
+        // keys seen by every row of tile t: ctx + t T + 1
+        pre_keys += (unsigned long long)nt * (ctx + 1) + (unsigned long long)T * nt * (nt - 1) / 2;
+        max_full = max(max_full, ctx + (nt - 1) * T + 1);
+      }
+    }
+    if (tiles) atomicAdd(&s_tiles, tiles);
+    if (max_full) atomicMax(&s_max_full, max_full);
+    if (pre_keys) atomicAdd(&s_pre_keys, pre_keys);
+    if (dec_keys) atomicAdd(&s_dec_keys, dec_keys);
   }
   __syncthreads();
   if (s_err) {
     if (tid == 0) {
       hdr[kHdrCounter] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
-      hdr[kHdrError] = 1; hdr[kHdrNumItems] = 0;
+      hdr[kHdrError] = 1; hdr[kHdrNumItems] = 0; hdr[kHdrPreSplitKeys] = 0; hdr[kHdrNumPreJobs] = 0;
     }
     return;
   }
-  // pass 2: per-sequence counts, block-wide exclusive scan (prefill count in the low 32 bits,
-  // decode count in the high 32 bits), emit entries
+  if (tid == 0) {
+    long long S = 0;
+    const long long H = p.num_kv_heads;
+    if (p.pre_slots > 0 && s_tiles > 0 && (long long)s_tiles * H <= kPlanComputeUnits) {
+      const long long pre_units = (long long)s_pre_keys * H;
+      const long long work = pre_units + pre_units / 2 + (long long)s_dec_keys * H;
+      const long long per_cu = (work + kPlanComputeUnits - 1) / kPlanComputeUnits;
+      S = max((long long)kMinSplitKeys, (pre_units + kPlanComputeUnits - 1) / kPlanComputeUnits);
+      S = max(S, (2 * per_cu + 2) / 3);
+      S = (S + kKeysPerStage - 1) / kKeysPerStage * kKeysPerStage;
+      if (S >= s_max_full) S = 0;            // no tile would split
+    }
+    s_split_keys = (int)S;
+  }
+  __syncthreads();
+  const int S = s_split_keys;
+  // pass 2: per-sequence counts (prefill entries, decode entries, split tiles), block-wide
+  // exclusive scans, then the entries: prefill tiles last (longest) tile first, splits in order
   for (int base = 0; base < p.batch; base += kPlanThreads) {
     const int b = base + tid;
-    int n_pre = 0, n_dec = 0, kind = kSeqNone, q_start = 0, q_len = 0, ctx = 0;
+    int cnt[3] = {0, 0, 0};
+    int kind = kSeqNone, q_start = 0, q_len = 0, ctx = 0, nt = 0;
     if (b < p.batch) {
       q_start = cu ? cu[b] : b;
       q_len = cu ? cu[b + 1] - q_start : 1;
@@ -173,48 +226,64 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         if (dec) {
           const int pages = (ctx + q_len + kPage - 1) / kPage;
           kind = kSeqDecode;
-          n_dec = (pages + p.pages_per_split - 1) / p.pages_per_split;
+          cnt[1] = (pages + p.pages_per_split - 1) / p.pages_per_split;
         } else {
           kind = kSeqPrefill;
-          n_pre = (q_len + p.tokens_per_tile - 1) / p.tokens_per_tile;
+          nt = (q_len + T - 1) / T;
+          for (int t = 0; t < nt; ++t) {
+            const int ns = tile_splits(ctx, t * T, S);
+            cnt[0] += ns;
+            cnt[2] += ns > 1;
+          }
         }
       }
     }
-    const long long v = (long long)n_pre | ((long long)n_dec << 32);
-    s_scan[tid] = v;
+    int excl[3];
+#pragma unroll
+    for (int c = 0; c < 3; ++c) s_scan[c][tid] = cnt[c];
     __syncthreads();
     for (int off = 1; off < kPlanThreads; off <<= 1) {
-      const long long add = tid >= off ? s_scan[tid - off] : 0;
+      int add[3];
+#pragma unroll
+      for (int c = 0; c < 3; ++c) add[c] = tid >= off ? s_scan[c][tid - off] : 0;
       __syncthreads();
-      s_scan[tid] += add;
+#pragma unroll
+      for (int c = 0; c < 3; ++c) s_scan[c][tid] += add[c];
       __syncthreads();
     }
-    const long long incl = s_scan[tid] + s_carry;
-    const long long excl = incl - v;
-    const int pre_off = (int)(excl & 0xffffffffLL);
-    const int dec_off = (int)(excl >> 32);
+#pragma unroll
+    for (int c = 0; c < 3; ++c) excl[c] = s_scan[c][tid] - cnt[c] + s_carry[c];
     if (b < p.batch) {
-      seqinfo[b] = SeqInfo{q_start, q_len, ctx, kind | (n_dec << 4)};
-      split_base[b] = dec_off;
-      // prefill tiles, last (longest) tile first
-      for (int t = 0; t < n_pre; ++t)
-        if (pre_off + t < p.max_pre) entries[pre_off + t] = make_int2(b, n_pre - 1 - t);
-      for (int s = 0; s < n_dec; ++s)
-        if (dec_off + s < p.max_dec) entries[p.max_pre + dec_off + s] = make_int2(b, s);
+      seqinfo[b] = SeqInfo{q_start, q_len, ctx, kind | (cnt[1] << 4)};
+      split_base[b] = excl[1];
+      int e = excl[0], j = excl[2];
+      for (int t = nt - 1; t >= 0; --t) {
+        const int ns = tile_splits(ctx, t * T, S);
+        if (ns > 1 && j < p.pre_jobs_cap) pre_jobs[j++] = make_int4(b, t, e, ns);
+        for (int sp = 0; sp < ns; ++sp, ++e)
+          if (e < p.max_pre) entries[e] = make_int2(b, t | (sp << 16));
+      }
+      for (int sp = 0; sp < cnt[1]; ++sp)
+        if (excl[1] + sp < p.max_dec) entries[p.max_pre + excl[1] + sp] = make_int2(b, sp);
     }
     __syncthreads();
-    if (tid == kPlanThreads - 1) s_carry = incl;
+    if (tid == kPlanThreads - 1) {
+#pragma unroll
+      for (int c = 0; c < 3; ++c) s_carry[c] = excl[c] + cnt[c];
+    }
     __syncthreads();
   }
   if (tid == 0) {
-    const int n_pre = (int)(s_carry & 0xffffffffLL);
-    const int n_dec = (int)(s_carry >> 32);
-    const bool over = n_pre > p.max_pre || n_dec > p.max_dec;
+    const int n_pre = s_carry[0], n_dec = s_carry[1], n_jobs = s_carry[2];
+    const bool over = n_pre > p.max_pre || n_dec > p.max_dec || n_jobs > p.pre_jobs_cap ||
+                      (n_jobs > 0 && (long long)n_pre * p.num_kv_heads > p.pre_slots);
     hdr[kHdrCounter] = 0;
     hdr[kHdrNumPre] = over ? 0 : n_pre;
     hdr[kHdrNumDec] = over ? 0 : n_dec;
     hdr[kHdrError] = over ? 2 : 0;
     hdr[kHdrNumItems] = over ? 0 : (n_pre + n_dec) * p.num_kv_heads;
+    hdr[kHdrPreSplitKeys] = S;
+    hdr[kHdrNumPreJobs] = over ? 0 : n_jobs;
   }
 }
 
@@ -226,9 +295,12 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 //   O^T (dims x rows) += V^T . P^T  (A = V^T via LDS transpose reads, B = P^T from S^T registers)
 // Each lane owns one q-row (l%32) for both products, so the softmax row statistics are
 // lane-local apart from one exchange with lane l^32, which holds the row's other keys.
+// A split item (entry e, code = tile | split << 16) covers only its key range and writes the
+// unnormalised (o~, m, l) of its rows to partial slot e * H_kv + g for the prefill merge.
 // ------------------------------------------------------------------------------------------------
 template <int D>
-__device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile, int g, char* smem) {
+__device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
+                                             char* smem) {
   constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
   constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
   constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
@@ -242,6 +314,7 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
   const SeqInfo si = a.seqinfo[b];
   const int G = a.group;
+  const int tile = code & 0xffff, split = code >> 16;
   const int t0 = tile * a.tokens_per_tile;
   const int t_end = min(t0 + a.tokens_per_tile, si.q_len);
   const int ctx = si.ctx_len;
@@ -272,6 +345,9 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
   float m_run = -INFINITY, l_run = 0.f;
 
   const int n_steps = (kv_needed + kKeysPerStage - 1) / kKeysPerStage;
+  const int n_split = tile_splits(ctx, t0, split_keys);
+  const int step_begin = split * (split_keys / kKeysPerStage);
+  const int step_end = split + 1 < n_split ? step_begin + split_keys / kKeysPerStage : n_steps;
 
   // K/V staging: chunk i of this thread is 16 bytes of key row kk = cidx / CPR of the stage; the
   // stage's page index of that row is the same for the whole wave, so it comes from a scalar
@@ -382,28 +458,42 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int b, int tile,
   };
 
   Stage sA, sB;
-  const int last_step = n_steps - 1;
-  load_stage(0, sA);
-  load_stage(min(1, last_step), sB);
-  store_stage(0, 0, sA);
+  const int last_step = step_end - 1;
+  load_stage(step_begin, sA);
+  load_stage(min(step_begin + 1, last_step), sB);
+  store_stage(step_begin, 0, sA);
   __syncthreads();
-  for (int step = 0; step < n_steps; step += 2) {
+  for (int step = step_begin; step < step_end; step += 2) {
     // even step: sB holds step+1 (in flight); refill sA with step+2 (past the end: a repeat)
     load_stage(min(step + 2, last_step), sA);
     compute(step, 0);
-    if (step + 1 < n_steps) store_stage(step + 1, 1, sB);
+    if (step + 1 < step_end) store_stage(step + 1, 1, sB);
     __syncthreads();
-    if (step + 1 >= n_steps) break;
+    if (step + 1 >= step_end) break;
     // odd step: sA holds step+2; refill sB with step+3
     load_stage(min(step + 3, last_step), sB);
     compute(step + 1, 1);
-    if (step + 2 < n_steps) store_stage(step + 2, 0, sA);
+    if (step + 2 < step_end) store_stage(step + 2, 0, sA);
     __syncthreads();
   }
 
-  // epilogue: combine the two half-row sums, normalise, store bf16 O and fp32 LSE
+  // epilogue: combine the two half-row sums; a split item stores its fp32 partial state
   const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (row_ok) {
+  if (row_ok && n_split > 1) {
+    const size_t prow = (size_t)(e * H_kv + g) * kRowsPerTile + rho;
+    float* po = a.part_pre_o + prow * D;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq)
+        *reinterpret_cast<f32x4*>(po + 32 * mb + 8 * rq + 4 * half) =
+            f32x4{oacc[mb][4 * rq + 0], oacc[mb][4 * rq + 1], oacc[mb][4 * rq + 2], oacc[mb][4 * rq + 3]};
+    if (half == 0) {
+      a.part_pre_ml[2 * prow] = m_run;
+      a.part_pre_ml[2 * prow + 1] = l_tot;
+    }
+  } else if (row_ok) {
+    // normalise, store bf16 O and fp32 LSE
     const float inv = 1.0f / l_tot;
     uint16_t* orow = a.out + ((size_t)(si.q_start + tok) * H_q + h) * D;
 #pragma unroll
@@ -701,6 +791,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   __shared__ int s_item[2];
   const int n_items = a.ws_hdr[kHdrNumItems];
   const int n_pre = a.ws_hdr[kHdrNumPre];
+  const int split_keys = a.ws_hdr[kHdrPreSplitKeys];
   const int H_kv = a.num_kv_heads;
   if (threadIdx.x == 0) s_item[0] = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
   __syncthreads();
@@ -714,7 +805,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
       if constexpr ((kKinds & 1) != 0) {
         static_assert(NW == kWaves, "prefill tiles use 8 waves");
         const int2 en = a.entries[e];
-        prefill_tile<D>(a, en.x, en.y, g, smem);
+        prefill_tile<D>(a, e, en.x, en.y, g, split_keys, smem);
       }
     } else {
       if constexpr ((kKinds & 2) != 0) {
@@ -766,6 +857,52 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a, int batch) {
 #pragma unroll
   for (int i = 0; i < PER; ++i) orow[i] = bf16_bits(acc[i] * inv);
   if (lane == 0 && a.lse) a.lse[(size_t)si.q_start * H_q + h] = (M + flog2(L)) * kLn2;
+}
+
+// ------------------------------------------------------------------------------------------------
+// Merge of split prefill tiles: one wave per (job, kv-head, tile row), grid-stride over the jobs
+// the planner recorded.  Same combination as the decode merge, over the tile's splits.
+// ------------------------------------------------------------------------------------------------
+constexpr int kMergeMaxBlocks = 4096;
+
+template <int D>
+__global__ __launch_bounds__(256) void merge_prefill_kernel(AttnArgs a) {
+  if (a.ws_hdr[kHdrError] != 0) return;
+  const int lane = threadIdx.x & 63;
+  const int H_kv = a.num_kv_heads, H_q = a.num_q_heads, G = a.group, T = a.tokens_per_tile;
+  const int total = a.ws_hdr[kHdrNumPreJobs] * H_kv * kRowsPerTile;
+  constexpr int PER = D / 64;
+  for (int r = blockIdx.x * 4 + (threadIdx.x >> 6); r < total; r += gridDim.x * 4) {
+    const int rho = r % kRowsPerTile, jg = r / kRowsPerTile;
+    const int g = jg % H_kv, j = jg / H_kv;
+    const int4 job = a.pre_jobs[j];                  // (sequence, tile, first entry, splits)
+    const SeqInfo si = a.seqinfo[job.x];
+    const int tok = job.y * T + rho / G;
+    if (tok >= si.q_len) continue;
+    const int h = g * G + rho % G;
+    const int ns = job.w;
+    float M = -INFINITY;
+    for (int sp = lane; sp < ns; sp += 64)
+      M = fmaxf(M, a.part_pre_ml[2 * ((size_t)((job.z + sp) * H_kv + g) * kRowsPerTile + rho)]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+    float acc[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) acc[i] = 0.f;
+    float L = 0.f;
+    for (int sp = 0; sp < ns; ++sp) {
+      const size_t prow = (size_t)((job.z + sp) * H_kv + g) * kRowsPerTile + rho;
+      const float f = fexp2(a.part_pre_ml[2 * prow] - M);
+      L += f * a.part_pre_ml[2 * prow + 1];
+#pragma unroll
+      for (int i = 0; i < PER; ++i) acc[i] += f * a.part_pre_o[prow * D + lane * PER + i];
+    }
+    const float inv = 1.0f / L;
+    const size_t orow = (size_t)(si.q_start + tok) * H_q + h;
+#pragma unroll
+    for (int i = 0; i < PER; ++i) a.out[orow * D + lane * PER + i] = bf16_bits(acc[i] * inv);
+    if (lane == 0 && a.lse) a.lse[orow] = (M + flog2(L)) * kLn2;
+  }
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -822,7 +959,8 @@ hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32
   char* ws = static_cast<char*>(workspace);
   hipLaunchKernelGGL(plan_kernel, dim3(1), dim3(kPlanThreads), 0, stream, p, ctx_lens, cu_q_lens,
                      reinterpret_cast<int32_t*>(ws + lay.hdr), reinterpret_cast<SeqInfo*>(ws + lay.seqinfo),
-                     reinterpret_cast<int32_t*>(ws + lay.split_base), reinterpret_cast<int2*>(ws + lay.entries));
+                     reinterpret_cast<int32_t*>(ws + lay.split_base), reinterpret_cast<int2*>(ws + lay.entries),
+                     reinterpret_cast<int4*>(ws + lay.pre_jobs));
   return hipGetLastError();
 }
 
@@ -855,6 +993,18 @@ hipError_t launch_merge(const AttnArgs& a, int head_dim, int batch, hipStream_t 
     hipLaunchKernelGGL(merge_kernel<64>, dim3(grid), dim3(256), 0, stream, a, batch);
   else
     hipLaunchKernelGGL(merge_kernel<128>, dim3(grid), dim3(256), 0, stream, a, batch);
+  return hipGetLastError();
+}
+
+hipError_t launch_merge_prefill(const AttnArgs& a, int head_dim, int64_t jobs_cap, hipStream_t stream) {
+  const int64_t waves = jobs_cap * a.num_kv_heads * kRowsPerTile;
+  int64_t grid = (waves + 3) / 4;
+  if (grid > kMergeMaxBlocks) grid = kMergeMaxBlocks;
+  if (grid <= 0) return hipSuccess;
+  if (head_dim == 64)
+    hipLaunchKernelGGL(merge_prefill_kernel<64>, dim3((unsigned)grid), dim3(256), 0, stream, a);
+  else
+    hipLaunchKernelGGL(merge_prefill_kernel<128>, dim3((unsigned)grid), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

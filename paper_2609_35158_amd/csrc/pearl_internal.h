@@ -18,6 +18,14 @@ constexpr int kMaxPagesPerSplit = 512;   // page ids of one split are staged in 
 // Compute units assumed when sizing decode splits (MI355X has 256).  A fixed value keeps the
 // workspace size a pure function of the shapes; the launch grid uses the device's real count.
 constexpr int kPlanComputeUnits = 256;
+// Prefill tiles are split along the keys only when the launch has few of them (at most one item
+// per compute unit); a split then holds at least kMinSplitKeys keys, and all split items of a
+// launch fit in kMaxPreSplitItems partial slots (kRowsPerTile rows each).
+constexpr int kMinSplitKeys = 1024;
+constexpr int kMaxPreSplitItems = 2 * kPlanComputeUnits;
+// Entry encoding of a prefill work item: y = tile | split << 16.
+constexpr int kMaxQLen = 1 << 21;        // tiles per sequence < 2^16 (>= 32 tokens per tile)
+constexpr int kMaxKvLen = 1 << 25;       // splits per tile < 2^15 (>= 1024 keys per split)
 
 enum Mode : int { kModePrefill = 0, kModeDecode = 1, kModeMixed = 2 };
 
@@ -31,6 +39,8 @@ enum Hdr : int {
   kHdrNumDec = 2,      // decode split entries
   kHdrError = 3,       // nonzero: a sequence violated the host bounds; nothing is computed
   kHdrNumItems = 4,    // (pre + dec) * H_kv
+  kHdrPreSplitKeys = 5,  // keys per prefill split (a multiple of 64); 0 = tiles are not split
+  kHdrNumPreJobs = 6,  // prefill tiles with more than one split (merge jobs)
   kHdrZero = 32,       // words 32..63: a zeroed 128-byte block (source for keys past the end)
   kHdrWords = 64
 };
@@ -45,8 +55,10 @@ struct SeqInfo {
 
 // Offsets (bytes) of the workspace regions; all 256-byte aligned.
 struct WsLayout {
-  size_t hdr, seqinfo, split_base, entries, part_o, part_ml, total;
+  size_t hdr, seqinfo, split_base, entries, part_o, part_ml, pre_jobs, part_pre_o, part_pre_ml, total;
   int64_t max_pre, max_dec;
+  int64_t pre_slots;     // partial slots for split prefill items (0: prefill tiles never split)
+  int64_t pre_jobs_cap;  // capacity of the prefill merge-job list
 };
 
 struct PlanParams {
@@ -62,6 +74,8 @@ struct PlanParams {
   int pages_per_split;
   int64_t max_pre;       // capacity of the prefill entry list
   int64_t max_dec;       // capacity of the decode entry list (and of the partial buffers)
+  int64_t pre_slots;     // partial slots for split prefill items
+  int64_t pre_jobs_cap;  // capacity of the prefill merge-job list
 };
 
 struct AttnArgs {
@@ -77,6 +91,9 @@ struct AttnArgs {
   const int2* entries;
   float* part_o;
   float* part_ml;
+  const int4* pre_jobs;      // (sequence, tile, first entry, splits) per split prefill tile
+  float* part_pre_o;         // [slot][kRowsPerTile][D] unnormalised partial outputs
+  float* part_pre_ml;        // [slot][kRowsPerTile][2] running max (log2 units) and sum
   int bt_stride;
   int num_pages;
   int num_q_heads;
@@ -88,7 +105,8 @@ struct AttnArgs {
 };
 
 WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_heads,
-                          int num_kv_heads, int head_dim, int group, int pages_per_split);
+                          int num_kv_heads, int head_dim, int group, int pages_per_split,
+                          bool has_prefill);
 int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu);
 int device_num_cu();
 
@@ -106,5 +124,8 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t 
                             hipStream_t stream);
 
 hipError_t launch_merge(const AttnArgs& a, int head_dim, int batch, hipStream_t stream);
+
+// Merge of split prefill tiles; jobs_cap bounds the device-side job count.
+hipError_t launch_merge_prefill(const AttnArgs& a, int head_dim, int64_t jobs_cap, hipStream_t stream);
 
 }  // namespace pearl

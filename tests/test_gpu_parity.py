@@ -314,3 +314,66 @@ def test_score_range_and_running_max(pattern):
     rows = [int(case.cu_q_lens[b]) for b in dec]
     assert_close(bits(out_d), o_ref[rows], lse_d.cpu().numpy(), l_ref[rows], what="%s decode" % pattern,
                  ulp_slack=2.0 if pattern == "large" else 0.0)
+
+
+def _attend_with_workspace(case, mode):
+    """Attention through the C ABI with a caller-owned workspace, returned for inspection."""
+    from paper_2609_35158_amd import binding as bd
+    ctx, cu = dev_lengths(case)
+    max_q, max_kv = bounds(case)
+    desc = bd.make_desc(case.block_table, ctx, cu, case.total_q, max_q, max_kv)
+    ws = torch.empty(bd.workspace_bytes(case.num_q_heads, case.k_pool, desc), dtype=torch.uint8, device="cuda")
+    fn = {"prefill": pa.prefill_append, "mixed": pa.mixed}[mode]
+    out, lse = fn(case.q, case.k_pool, case.v_pool, case.block_table, ctx, cu, max_q, max_kv,
+                  scale=case.scale, return_lse=True, workspace=ws)
+    return out, lse, ws
+
+
+PREFILL_SPLIT_CASES = [
+    # (G, H_kv, d, contexts, chunk lengths, modes)
+    (8, 4, 128, [8000], [100], ("prefill", "mixed")),
+    (4, 2, 64, [3000, 1500], [60, 5], ("prefill", "mixed")),
+    (1, 1, 128, [2500], [300], ("prefill", "mixed")),
+    (2, 8, 128, [5000, 0, 2000], [33, 17, 1], ("prefill", "mixed")),
+    (8, 1, 64, [1030, 4097], [1, 250], ("prefill",)),
+]
+
+
+@pytest.mark.parametrize("idx", range(len(PREFILL_SPLIT_CASES)))
+def test_prefill_key_splits(idx):
+    """Few prefill tiles on long contexts: the planner splits each tile's keys (checked in the
+    workspace header) and the prefill merge combines the partial states; outputs and LSE against
+    the oracle.  Contexts end mid-page and chunks span ragged tiles."""
+    G, H_kv, d, ctx, ql, modes = PREFILL_SPLIT_CASES[idx]
+    say("case: prefill key splits G=%d H_kv=%d d=%d ctx=%s q=%s" % (G, H_kv, d, ctx, ql))
+    case = workloads.build_case("pre-split", 9100 + idx, H_kv * G, H_kv, d, np.array(ctx), np.array(ql),
+                                device="cuda", extra_pages=2)
+    kr, vr = _append_and_check(case)
+    o_ref, l_ref = oracle_full(case, kr, vr)
+    for mode in modes:
+        out, lse, ws = _attend_with_workspace(case, mode)
+        torch.cuda.synchronize()
+        hdr = ws[:64 * 4].view(torch.int32).cpu().numpy()
+        say("   %s: keys per split %d, split tiles %d" % (mode, hdr[5], hdr[6]))
+        if mode == "prefill":
+            assert hdr[5] > 0 and hdr[6] > 0, "expected the planner to split prefill tiles"
+        assert hdr[3] == 0
+        assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="%s split case %d" % (mode, idx))
+
+
+def test_prefill_key_splits_long_context_sampled():
+    """One 256-token chunk on a 30000-token context (Qwen3-30B-A3B shape): splits larger than the
+    minimum; sampled tokens against the oracle."""
+    from gpu_helpers import oracle_sampled
+    say("case: prefill key splits, 256 tokens on 30000")
+    case = workloads.build_case("pre-split-long", 9200, 32, 4, 128, np.array([30000]), np.array([256]),
+                                device="cuda")
+    gpu_append(case)
+    out, lse, ws = _attend_with_workspace(case, "prefill")
+    torch.cuda.synchronize()
+    hdr = ws[:64 * 4].view(torch.int32).cpu().numpy()
+    say("   keys per split %d, split tiles %d" % (hdr[5], hdr[6]))
+    assert hdr[5] > 1024 and hdr[6] == 8
+    toks = [0, 1, 31, 32, 100, 200, 254, 255]
+    o_ref, l_ref = oracle_sampled(case, [0], {0: toks})
+    assert_close(bits(out)[toks], o_ref[0][toks], lse.cpu().numpy()[toks], l_ref[0][toks], what="long split")
