@@ -30,8 +30,8 @@
  *   - `stream` is a hipStream_t (NULL = the null stream).  Calls are asynchronous on it; the
  *     library allocates no device memory, keeps no pointer after returning and holds no state
  *     between calls apart from per-device launch parameters queried once.
- *   - Supported: head_dim 64 or 128; page_size 16; G = num_q_heads/num_kv_heads in {1,2,4,8}.
- *     Anything else returns PEARL_ERR_UNSUPPORTED.
+ *   - Supported: head_dim 64 or 128; page_size 16; G = num_q_heads/num_kv_heads in {1,2,4,8};
+ *     max_q_len <= 2^21 and max_kv_len <= 2^25.  Anything else returns PEARL_ERR_UNSUPPORTED.
  *   - Host-checkable errors (NULL pointers, bad shapes, batch <= 0, sizes inconsistent with each
  *     other, misaligned pointers, workspace too small) return synchronously before any HIP call.
  *     A HIP launch error returns PEARL_ERR_HIP.  The failing detail is in pearl_last_error().
@@ -115,7 +115,11 @@ pearl_status pearl_kv_append(const pearl_kv_shape* shape, const pearl_seq_desc* 
  * Bytes of device workspace that any of the three attention calls below needs for (shape,
  * seqs).  The workspace holds the device-built work list and the split-context partial results
  * (fp32); it needs no initialisation and its contents after a call are unspecified.  Returns 0
- * if the arguments are invalid (pearl_last_error() says why).
+ * if the arguments are invalid (pearl_last_error() says why).  The size is a function of the
+ * shape and the host bounds only.  Decode partials take batch * ceil(pages / split) *
+ * num_q_heads * (head_dim + 2) floats.  When cu_q_lens is non-NULL and max_kv_len > 1024,
+ * partials of key-split prefill tiles add up to 512 * 256 * (head_dim + 2) floats (65 MiB at
+ * head_dim 128).
  */
 size_t pearl_attn_workspace_bytes(const pearl_kv_shape* shape, const pearl_seq_desc* seqs);
 
@@ -125,6 +129,8 @@ size_t pearl_attn_workspace_bytes(const pearl_kv_shape* shape, const pearl_seq_d
  * every sequence attends causally within its chunk and fully to the cached context; the pools
  * must already hold the new tokens' K/V (call pearl_kv_append first, on the same stream).
  * Sequences with zero new tokens are skipped.  Uses bf16 MFMA tiles with an fp32 online softmax.
+ * When a launch has few tiles on long contexts, each tile's keys are split into ranges that run
+ * in parallel and are merged by log-sum-exp (decided on the device from the actual lengths).
  *   q: bf16 [total_q][H_q][d] (read); out: bf16 [total_q][H_q][d] (written);
  *   lse: fp32 [total_q][H_q] natural-log log-sum-exp of the scaled scores, or NULL;
  *   softmax_scale: the scale applied to q.k (normally 1/sqrt(d)), > 0 and finite;
