@@ -139,6 +139,40 @@ def kv_append(k_pool: np.ndarray, v_pool: np.ndarray, k_new: np.ndarray, v_new: 
 
 
 # ------------------------------------------------------------------------------------------
+# KV transfer between pools (PD disaggregation: the prefill pool hands each turn's new-token
+# K/V to the decode pool; section 4.3, Eq. 3, the B * dL * K / BW transfer term)
+# ------------------------------------------------------------------------------------------
+
+def kv_pack(k_pool: np.ndarray, v_pool: np.ndarray, block_table: np.ndarray, ctx_lens: np.ndarray,
+            cu_q_lens: Optional[np.ndarray]) -> np.ndarray:
+    """Gather token rows out of the pools into a contiguous transfer buffer.
+
+    For sequence b the rows of positions ctx_lens[b] .. ctx_lens[b] + n_b - 1 (n_b from
+    cu_q_lens; one row each when it is None) go to buffer rows cu_q_lens[b] + t, for every
+    kv-head.  Returns uint16 [2][total][H_kv][d]: K rows, then V rows."""
+    B = len(ctx_lens)
+    ql = _q_lens(cu_q_lens, B)
+    qs = _q_starts(cu_q_lens, B)
+    total = int(ql.sum())
+    H_kv, d = k_pool.shape[1], k_pool.shape[3]
+    buf = np.zeros((2, total, H_kv, d), dtype=np.uint16)
+    for b in range(B):
+        row = np.asarray(block_table[b])
+        for t in range(int(ql[b])):
+            page, slot = _page_slot(row, np.int64(int(ctx_lens[b]) + t))
+            buf[0, qs[b] + t] = k_pool[int(page), :, int(slot), :]
+            buf[1, qs[b] + t] = v_pool[int(page), :, int(slot), :]
+    return buf
+
+
+def kv_unpack(k_pool: np.ndarray, v_pool: np.ndarray, buf: np.ndarray, block_table: np.ndarray,
+              ctx_lens: np.ndarray, cu_q_lens: Optional[np.ndarray]) -> Tuple[np.ndarray, np.ndarray]:
+    """Scatter a transfer buffer (as made by kv_pack) into pools with their own block table:
+    the append of its K half and V half at positions ctx_lens[b] + t."""
+    return kv_append(k_pool, v_pool, buf[0], buf[1], block_table, ctx_lens, cu_q_lens)
+
+
+# ------------------------------------------------------------------------------------------
 # attention over the paged cache
 # ------------------------------------------------------------------------------------------
 

@@ -356,4 +356,68 @@ def pin_bf16_rounding():
     assert abs(oracle.bf16_bits_to_f64(b[4:5])[0] - 0.1) <= 2 ** -4 * 2 ** -8
 
 
+def pin_kv_pack_closed_form():
+    """Pools whose every row encodes its own address (K: page, head, slot, 0; V: the negatives
+    minus one): packed row cu[b] + t of kv-head h must read (bt[b][p // 16], h, p % 16) with
+    p = ctx[b] + t.  All codes are small integers, exact in bf16."""
+    rng = np.random.default_rng(23)
+    H_kv, d = 3, 4
+    ctx = np.array([0, 15, 16, 40, 7])
+    ql = np.array([17, 2, 16, 0, 1])
+    bt, num_pages = rand_layout(rng, ctx + ql, extra=2)
+    code = np.zeros((num_pages, H_kv, PAGE, d), dtype=np.float32)
+    code[..., 0] = np.arange(num_pages)[:, None, None]
+    code[..., 1] = np.arange(H_kv)[None, :, None]
+    code[..., 2] = np.arange(PAGE)[None, None, :]
+    kp, vp = bits(code), bits(-code - 1)
+    cu = np.concatenate([[0], np.cumsum(ql)]).astype(np.int32)
+    buf = pa.kv_pack(kp, vp, bt, ctx, cu)
+    assert buf.shape == (2, int(ql.sum()), H_kv, d)
+    got_k = oracle.bf16_bits_to_f64(buf[0])
+    got_v = oracle.bf16_bits_to_f64(buf[1])
+    for b in range(len(ctx)):
+        for t in range(ql[b]):
+            p = ctx[b] + t
+            for h in range(H_kv):
+                want = np.array([bt[b][p // PAGE], h, p % PAGE, 0.0])
+                assert np.array_equal(got_k[cu[b] + t, h], want), (b, t, h)
+                assert np.array_equal(got_v[cu[b] + t, h], -want - 1), (b, t, h)
+    # one row per sequence when cu_q_lens is None: row b holds position ctx[b]
+    one = pa.kv_pack(kp, vp, bt, ctx, None)
+    for b in range(len(ctx)):
+        p = ctx[b]
+        assert np.array_equal(oracle.bf16_bits_to_f64(one[0, b, 2]), [bt[b][p // PAGE], 2, p % PAGE, 0.0])
+
+
+def pin_kv_pack_unpack_transfer():
+    """A transfer between two pools with different page placements: packing token ranges out of
+    pool A and unpacking them into pool B makes B's gathered rows equal A's, leaves every other
+    byte of B unchanged, and packing B again returns the same buffer."""
+    rng = np.random.default_rng(29)
+    H_kv, d = 2, 8
+    ctx = np.array([3, 33, 0])
+    ql = np.array([30, 1, 16])
+    lens = ctx + ql
+    bt_a, np_a = rand_layout(rng, lens, extra=1)
+    bt_b, np_b = rand_layout(rng, lens, extra=5)
+    kp_a = rng.integers(0, 65536, size=(np_a, H_kv, PAGE, d)).astype(np.uint16)
+    vp_a = rng.integers(0, 65536, size=(np_a, H_kv, PAGE, d)).astype(np.uint16)
+    kp_b = rng.integers(0, 65536, size=(np_b, H_kv, PAGE, d)).astype(np.uint16)
+    vp_b = rng.integers(0, 65536, size=(np_b, H_kv, PAGE, d)).astype(np.uint16)
+    cu = np.concatenate([[0], np.cumsum(ql)]).astype(np.int32)
+    buf = pa.kv_pack(kp_a, vp_a, bt_a, ctx, cu)
+    kb2, vb2 = pa.kv_unpack(kp_b, vp_b, buf, bt_b, ctx, cu)
+    touched = np.zeros((np_b, PAGE), dtype=bool)
+    for b in range(len(ctx)):
+        for p in range(ctx[b], lens[b]):
+            pa_, pb_, sl = bt_a[b][p // PAGE], bt_b[b][p // PAGE], p % PAGE
+            assert np.array_equal(kb2[pb_, :, sl, :], kp_a[pa_, :, sl, :])
+            assert np.array_equal(vb2[pb_, :, sl, :], vp_a[pa_, :, sl, :])
+            touched[pb_, sl] = True
+    keep = ~touched
+    assert np.array_equal(kb2.transpose(0, 2, 1, 3)[keep], kp_b.transpose(0, 2, 1, 3)[keep])
+    assert np.array_equal(vb2.transpose(0, 2, 1, 3)[keep], vp_b.transpose(0, 2, 1, 3)[keep])
+    assert np.array_equal(pa.kv_pack(kb2, vb2, bt_b, ctx, cu), buf)
+
+
 ALL_PINS = [v for k, v in sorted(globals().items()) if k.startswith("pin_")]

@@ -46,6 +46,17 @@ def _merge_drops_rescale(states):
     return acc / l_star, m_star + np.log(l_star)
 
 
+_orig_pack = pa.kv_pack
+
+
+def _pack_k_v_swapped(k_pool, v_pool, block_table, ctx_lens, cu_q_lens):
+    return _orig_pack(k_pool, v_pool, block_table, ctx_lens, cu_q_lens)[::-1]
+
+
+def _pack_rows_shifted(k_pool, v_pool, block_table, ctx_lens, cu_q_lens):
+    return _orig_pack(k_pool, v_pool, block_table, np.asarray(ctx_lens) + 1, cu_q_lens)
+
+
 MUTATIONS = {
     "gqa_mod_instead_of_div": ("_kv_head_of", lambda h, group: h % group),
     "exclusive_causal_mask": ("_visible", lambda ctx_len, i: ctx_len + i),
@@ -58,6 +69,8 @@ MUTATIONS = {
     "v_operand_is_k": ("gather_kv", _gather_v_is_k),
     "lse_missing_max": ("attention_unit", _unit_lse_without_max),
     "merge_without_rescale": ("merge_states", _merge_drops_rescale),
+    "pack_k_v_swapped": ("kv_pack", _pack_k_v_swapped),
+    "pack_rows_shifted": ("kv_pack", _pack_rows_shifted),
 }
 
 
