@@ -12,8 +12,9 @@ The same line carries:
                 events around each launch inside the timed region;
   cpu_baseline  the CPU oracle (numpy float64) timed on this host on a bounded sample;
   secondary     prefill-append TFLOP/s (Qwen3-8B shape), Qwen3-30B-A3B-shaped decode at batch
-                256/128/32, the colocated mixed batch, kv_append GB/s, and a decode/prefill
-                interference sweep (one mixed launch vs decode alone as prefill chunks grow).
+                256/128/32, the colocated mixed batch, kv_append GB/s, KV transfer pack/unpack
+                GB/s, and a decode/prefill interference sweep (one mixed launch vs decode alone
+                as prefill chunks grow).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-secondary] [--no-cpu]
 """
@@ -256,6 +257,56 @@ def pd_interference(torch, pa, workloads, steps, warmup):
 
 
 # ------------------------------------------------------------------------------------------------
+# KV transfer between pools (pack on the sending pool, unpack into the receiving pool)
+# ------------------------------------------------------------------------------------------------
+
+def kv_transfer(torch, pa, workloads, steps, warmup):
+    """Pack/unpack GB/s (algorithmic bytes = rows read + rows written) for two transfers on the
+    Qwen3-8B shape: whole contexts of the 64-sequence decode batch (2.4 GB of K/V, e.g. moving
+    trajectories between decode workers), and one turn's new tokens of the 16-sequence
+    prefill-append batch (the per-turn hand-off from prefill to decode pool, Eq. 3)."""
+    import numpy as np
+    out = []
+    for name, gen, whole in (("kv-transfer-full-context", lambda: workloads.qwen3_8b_decode("cuda"), True),
+                             ("kv-transfer-turn", lambda: workloads.qwen3_8b_prefill_append("cuda"), False)):
+        case = gen()
+        B = case.batch
+        if whole:
+            start, n = np.zeros(B, np.int64), case.ctx_lens.astype(np.int64)
+        else:
+            start, n = case.ctx_lens.astype(np.int64), case.q_lens.astype(np.int64)
+            fill, _ = make_step(torch, pa, case, "prefill")
+            fill(lambda: None, attention=False)
+        cu = np.concatenate([[0], np.cumsum(n)]).astype(np.int32)
+        total = int(cu[-1])
+        max_q, max_kv = int(n.max()), int((start + n).max())
+        st_d = torch.from_numpy(start.astype(np.int32)).cuda()
+        cu_d = torch.from_numpy(cu).cuda()
+        rng = np.random.default_rng(3)
+        perm = torch.from_numpy(rng.permutation(case.num_pages).astype(np.int64)).cuda()
+        bt_b = perm[case.block_table.long()].to(torch.int32).contiguous()   # another placement
+        kp_b, vp_b = torch.empty_like(case.k_pool), torch.empty_like(case.v_pool)
+        buf = torch.empty((2, total) + tuple(case.k_new.shape[1:]), dtype=torch.bfloat16, device="cuda")
+        pack = lambda hook: (hook(), pa.kv_pack(case.k_pool, case.v_pool, case.block_table, st_d, cu_d,
+                                                total, max_q, max_kv, out=buf))
+        unpack = lambda hook: (hook(), pa.kv_unpack(buf, kp_b, vp_b, bt_b, st_d, cu_d, max_q, max_kv))
+        _, ms_pack = run_timed(torch, pa, pack, steps, warmup)
+        _, ms_unpack = run_timed(torch, pa, unpack, steps, warmup)
+        moved = 2 * buf.numel() * 2            # read + write, bytes
+        e = {"workload": name, "mode": "kv-transfer", "tokens": total, "buffer_bytes": buf.numel() * 2,
+             "pack_ms": round(ms_pack, 5), "unpack_ms": round(ms_unpack, 5),
+             "pack_GBps": round(moved / (ms_pack * 1e-3) / 1e9, 1),
+             "unpack_GBps": round(moved / (ms_unpack * 1e-3) / 1e9, 1)}
+        e["frac_hbm_pack"] = round(e["pack_GBps"] / HBM_PEAK_GBPS, 4)
+        e["frac_hbm_unpack"] = round(e["unpack_GBps"] / HBM_PEAK_GBPS, 4)
+        log("bench:   %s" % json.dumps(e))
+        out.append(e)
+        del case, kp_b, vp_b, buf, bt_b, perm
+        torch.cuda.empty_cache()
+    return out
+
+
+# ------------------------------------------------------------------------------------------------
 # CPU oracle baseline on a bounded sample
 # ------------------------------------------------------------------------------------------------
 
@@ -469,6 +520,9 @@ def main():
             sec.append(entry)
             del c, st, o
             torch.cuda.empty_cache()
+        if not only or "kv-transfer" in only:
+            log("bench: secondary kv-transfer")
+            sec.extend(kv_transfer(torch, pa, workloads, args.steps, args.warmup))
         if not only or "pd-interference" in only:
             log("bench: secondary pd-interference")
             sec.append(pd_interference(torch, pa, workloads, max(5, args.steps // 2), args.warmup))

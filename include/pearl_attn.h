@@ -169,10 +169,31 @@ pearl_status pearl_attn_mixed(const pearl_kv_shape* shape, const pearl_seq_desc*
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * KV transfer between pools (paper, section 4.3, Eq. 3: under PD disaggregation the prefill
+ * pool hands each turn's new-token K/V to the decode pool; the transfer takes B * dL * K / BW).
+ * pearl_kv_pack gathers, for every sequence b, the K and V rows of positions ctx_lens[b] ..
+ * ctx_lens[b] + n_b - 1 (n_b from cu_q_lens, 1 when it is NULL) out of the pools into a
+ * contiguous buffer: row cu_q_lens[b] + t holds position ctx_lens[b] + t, for every kv-head.
+ * pearl_kv_unpack writes such a buffer into pools through their own block table (it is
+ * pearl_kv_append of the buffer's two halves), so the receiving pool may place the pages
+ * anywhere.  Both are bit copies; max_q_len bounds n_b and max_kv_len bounds ctx_lens[b] + n_b.
+ *   buf: bf16 [2][total_q][num_kv_heads][head_dim]: K rows, then V rows (pack writes it, unpack
+ *        reads it); 16-byte aligned.
+ *   k_pool, v_pool: as for pearl_kv_append (pack reads them, unpack writes them).
+ * A pack reading a page id outside [0, num_pages) writes zeros for those rows; an unpack skips
+ * them.  No other byte of buf (pack) or of the pools (unpack) changes.
+ */
+pearl_status pearl_kv_pack(const pearl_kv_shape* shape, const pearl_seq_desc* seqs,
+                           const void* k_pool, const void* v_pool, void* buf, void* stream);
+pearl_status pearl_kv_unpack(const pearl_kv_shape* shape, const pearl_seq_desc* seqs,
+                             const void* buf, void* k_pool, void* v_pool, void* stream);
+
+/*
  * Timing hook for benchmarks and profilers (not part of the computation).  While a pair is set,
  * every library call made on the calling thread records `before` on its stream immediately
  * before launching its main kernel (the attention kernel for the three attention calls, the
- * scatter kernel for pearl_kv_append) and `after` immediately after it.  The handles are
+ * page-copy kernel for pearl_kv_append, pearl_kv_pack and pearl_kv_unpack) and `after`
+ * immediately after it.  The handles are
  * hipEvent_t values created and owned by the caller; pass NULL, NULL to clear.  The pair stays
  * set until changed, so a caller timing several calls sets a fresh pair before each one.
  */

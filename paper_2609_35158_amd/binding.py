@@ -41,7 +41,7 @@ class SeqDesc(ctypes.Structure):
 
 EXPORTED = ("pearl_abi_version", "pearl_status_str", "pearl_last_error", "pearl_kv_append",
             "pearl_attn_workspace_bytes", "pearl_attn_prefill_append", "pearl_attn_decode",
-            "pearl_attn_mixed", "pearl_set_kernel_events")
+            "pearl_attn_mixed", "pearl_kv_pack", "pearl_kv_unpack", "pearl_set_kernel_events")
 
 
 def load(path: str = LIB_PATH):
@@ -63,6 +63,11 @@ def load(path: str = LIB_PATH):
     lib.pearl_kv_append.restype = ctypes.c_int
     lib.pearl_kv_append.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p,
                                     ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    for name in ("pearl_kv_pack", "pearl_kv_unpack"):
+        f = getattr(lib, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                      ctypes.c_void_p]
     lib.pearl_attn_workspace_bytes.restype = ctypes.c_size_t
     lib.pearl_attn_workspace_bytes.argtypes = [P(KvShape), P(SeqDesc)]
     for name in ("pearl_attn_prefill_append", "pearl_attn_decode", "pearl_attn_mixed"):
@@ -164,6 +169,43 @@ def kv_append(k_new: torch.Tensor, v_new: torch.Tensor, k_pool: torch.Tensor, v_
     st = load().pearl_kv_append(ctypes.byref(shape), ctypes.byref(desc), k_new.data_ptr(),
                                 v_new.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), _stream())
     _check(st, "pearl_kv_append")
+
+
+def kv_pack(k_pool: torch.Tensor, v_pool: torch.Tensor, block_table: torch.Tensor, ctx_lens: torch.Tensor,
+            cu_q_lens: Optional[torch.Tensor], total: int, max_q_len: int, max_kv_len: int,
+            out: Optional[torch.Tensor] = None) -> torch.Tensor:
+    """Gather token ranges [ctx_lens[b], ctx_lens[b] + n_b) of every sequence out of the pools into
+    a transfer buffer bf16 [2][total][H_kv][d] (pearl_kv_pack)."""
+    for t, n in ((k_pool, "k_pool"), (v_pool, "v_pool")):
+        _need(t, n, torch.bfloat16)
+    H_kv, d = int(k_pool.shape[1]), int(k_pool.shape[3])
+    if out is None:
+        out = torch.empty((2, total, H_kv, d), dtype=torch.bfloat16, device=k_pool.device)
+    _need(out, "out", torch.bfloat16)
+    if tuple(out.shape) != (2, total, H_kv, d):
+        raise ValueError("out must have shape (2, %d, %d, %d)" % (total, H_kv, d))
+    desc = make_desc(block_table, ctx_lens, cu_q_lens, total, max_q_len, max_kv_len)
+    shape = make_shape(H_kv, k_pool)
+    st = load().pearl_kv_pack(ctypes.byref(shape), ctypes.byref(desc), k_pool.data_ptr(), v_pool.data_ptr(),
+                              out.data_ptr(), _stream())
+    _check(st, "pearl_kv_pack")
+    return out
+
+
+def kv_unpack(buf: torch.Tensor, k_pool: torch.Tensor, v_pool: torch.Tensor, block_table: torch.Tensor,
+              ctx_lens: torch.Tensor, cu_q_lens: Optional[torch.Tensor], max_q_len: int,
+              max_kv_len: int) -> None:
+    """Scatter a transfer buffer bf16 [2][total][H_kv][d] into the pools at positions
+    ctx_lens[b] + t through this pool's block table (pearl_kv_unpack)."""
+    for t, n in ((buf, "buf"), (k_pool, "k_pool"), (v_pool, "v_pool")):
+        _need(t, n, torch.bfloat16)
+    if buf.dim() != 4 or buf.shape[0] != 2:
+        raise ValueError("buf must have shape (2, total, H_kv, d)")
+    desc = make_desc(block_table, ctx_lens, cu_q_lens, int(buf.shape[1]), max_q_len, max_kv_len)
+    shape = make_shape(k_pool.shape[1], k_pool)
+    st = load().pearl_kv_unpack(ctypes.byref(shape), ctypes.byref(desc), buf.data_ptr(), k_pool.data_ptr(),
+                                v_pool.data_ptr(), _stream())
+    _check(st, "pearl_kv_unpack")
 
 
 def _attention(fname: str, q: torch.Tensor, k_pool: torch.Tensor, v_pool: torch.Tensor,

@@ -295,6 +295,54 @@ pearl_status pearl_kv_append(const pearl_kv_shape* shape, const pearl_seq_desc* 
   }
 }
 
+pearl_status pearl_kv_pack(const pearl_kv_shape* shape, const pearl_seq_desc* seqs, const void* k_pool,
+                           const void* v_pool, void* buf, void* stream) {
+  try {
+    g_err[0] = 0;
+    pearl_status st = check_shape(shape);
+    if (st != PEARL_OK) return st;
+    st = check_seqs(seqs, false);
+    if (st != PEARL_OK) return st;
+    if (seqs->total_q == 0) return PEARL_OK;
+    if (!k_pool || !v_pool || !buf) return fail(PEARL_ERR_INVALID_ARG, "k_pool, v_pool and buf must be non-NULL");
+    if (!aligned16(k_pool) || !aligned16(v_pool) || !aligned16(buf))
+      return fail(PEARL_ERR_INVALID_ARG, "k_pool, v_pool and buf must be 16-byte aligned");
+    hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
+    uint16_t* k_rows = static_cast<uint16_t*>(buf);
+    uint16_t* v_rows = k_rows + (size_t)seqs->total_q * shape->num_kv_heads * shape->head_dim;
+    hipError_t e = record_before(hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
+    e = launch_kv_pack(static_cast<const uint16_t*>(k_pool), static_cast<const uint16_t*>(v_pool), k_rows, v_rows,
+                       seqs->block_table, seqs->bt_stride, seqs->ctx_lens, seqs->cu_q_lens, seqs->batch,
+                       seqs->max_q_len, shape->num_kv_heads, shape->head_dim, shape->num_pages, seqs->total_q, hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "kv_pack launch: %s", hipGetErrorString(e));
+    e = record_after(hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
+    return PEARL_OK;
+  } catch (...) {
+    return fail(PEARL_ERR_HIP, "unexpected exception in pearl_kv_pack");
+  }
+}
+
+pearl_status pearl_kv_unpack(const pearl_kv_shape* shape, const pearl_seq_desc* seqs, const void* buf,
+                             void* k_pool, void* v_pool, void* stream) {
+  try {
+    g_err[0] = 0;
+    pearl_status st = check_shape(shape);
+    if (st != PEARL_OK) return st;
+    st = check_seqs(seqs, false);
+    if (st != PEARL_OK) return st;
+    if (seqs->total_q == 0) return PEARL_OK;
+    if (!buf) return fail(PEARL_ERR_INVALID_ARG, "buf must be non-NULL");
+    // the unpack is the append of the buffer's K half and V half
+    const uint16_t* k_rows = static_cast<const uint16_t*>(buf);
+    const uint16_t* v_rows = k_rows + (size_t)seqs->total_q * shape->num_kv_heads * shape->head_dim;
+    return pearl_kv_append(shape, seqs, k_rows, v_rows, k_pool, v_pool, stream);
+  } catch (...) {
+    return fail(PEARL_ERR_HIP, "unexpected exception in pearl_kv_unpack");
+  }
+}
+
 void pearl_set_kernel_events(void* before, void* after) {
   g_ev_before = reinterpret_cast<hipEvent_t>(before);
   g_ev_after = reinterpret_cast<hipEvent_t>(after);

@@ -1,4 +1,4 @@
-// gfx950 (MI355X) kernels for paged-KV GQA attention: kv_append scatter, the device-side work
+// gfx950 (MI355X) kernels for paged-KV GQA attention: the device-side work
 // planner, the persistent attention kernel (prefill-append tiles on bf16 MFMA and split-context
 // decode items in one grid), and the split merge.
 //
@@ -84,42 +84,6 @@ template <int D, int NW, int kKinds> struct Lds {
   static constexpr int bytes0 = prefill_bytes > decode_bytes ? prefill_bytes : decode_bytes;
   static constexpr int bytes = bytes0 > 16 ? bytes0 : 16;
 };
-
-// ------------------------------------------------------------------------------------------------
-// kv_append: each thread copies one 16-byte chunk of a (token, kv-head) row of K and of V.
-// ------------------------------------------------------------------------------------------------
-constexpr int kAppendTokensPerBlock = 16;
-
-__global__ __launch_bounds__(256) void kv_append_kernel(
-    const u32x4* __restrict__ k_new, const u32x4* __restrict__ v_new, u32x4* __restrict__ k_pool,
-    u32x4* __restrict__ v_pool, const int32_t* __restrict__ bt, int bt_stride,
-    const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ cu, int num_kv_heads,
-    int chunks_per_row, int num_pages, int total_q) {
-  const int b = blockIdx.y;
-  const int t0 = blockIdx.x * kAppendTokensPerBlock;
-  const int q_start = cu ? cu[b] : b;
-  const int q_len = cu ? cu[b + 1] - q_start : 1;
-  const int ctx = ctx_lens[b];
-  const int n_tok = min(kAppendTokensPerBlock, q_len - t0);
-  if (n_tok <= 0 || q_start < 0 || ctx < 0) return;
-  const int per_tok = num_kv_heads * chunks_per_row;
-  const int total = n_tok * per_tok;
-  for (int i = threadIdx.x; i < total; i += blockDim.x) {
-    const int t = t0 + i / per_tok;
-    const int rem = i - (i / per_tok) * per_tok;
-    const int h = rem / chunks_per_row;
-    const int c = rem - h * chunks_per_row;
-    const int pos = ctx + t;
-    const int lp = pos / kPage;
-    if (lp >= bt_stride || q_start + t >= total_q) continue;
-    const int page = bt[(size_t)b * bt_stride + lp];
-    if (page < 0 || page >= num_pages) continue;
-    const size_t src = ((size_t)(q_start + t) * num_kv_heads + h) * chunks_per_row + c;
-    const size_t dst = (((size_t)page * num_kv_heads + h) * kPage + (pos % kPage)) * chunks_per_row + c;
-    k_pool[dst] = k_new[src];
-    v_pool[dst] = v_new[src];
-  }
-}
 
 // ------------------------------------------------------------------------------------------------
 // Planner: one workgroup validates the device-resident lengths against the host bounds and
@@ -939,20 +903,6 @@ DevCache& dev_cache() {
 }  // namespace
 
 int device_num_cu() { return dev_cache().num_cu; }
-
-hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
-                              uint16_t* v_pool, const int32_t* block_table, int bt_stride,
-                              const int32_t* ctx_lens, const int32_t* cu_q_lens, int batch,
-                              int max_q_len, int num_kv_heads, int head_dim, int num_pages,
-                              int total_q, hipStream_t stream) {
-  if (max_q_len <= 0 || batch <= 0) return hipSuccess;
-  dim3 grid((max_q_len + kAppendTokensPerBlock - 1) / kAppendTokensPerBlock, batch);
-  hipLaunchKernelGGL(kv_append_kernel, grid, dim3(256), 0, stream,
-                     reinterpret_cast<const u32x4*>(k_new), reinterpret_cast<const u32x4*>(v_new),
-                     reinterpret_cast<u32x4*>(k_pool), reinterpret_cast<u32x4*>(v_pool), block_table,
-                     bt_stride, ctx_lens, cu_q_lens, num_kv_heads, head_dim / 8, num_pages, total_q);
-  return hipGetLastError();
-}
 
 hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32_t* cu_q_lens,
                        void* workspace, const WsLayout& lay, hipStream_t stream) {

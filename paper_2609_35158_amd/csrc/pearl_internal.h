@@ -1,5 +1,5 @@
 // Internal interface between the C-ABI host layer (api.cpp) and the gfx950 kernels
-// (attn_kernels.hip).  Not installed; callers use include/pearl_attn.h.
+// (attn_kernels.hip, kv_pages.hip).  Not installed; callers use include/pearl_attn.h.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -115,6 +115,11 @@ hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16
                             const int32_t* ctx_lens, const int32_t* cu_q_lens, int batch,
                             int max_q_len, int num_kv_heads, int head_dim, int num_pages,
                             int total_q, hipStream_t stream);
+
+hipError_t launch_kv_pack(const uint16_t* k_pool, const uint16_t* v_pool, uint16_t* k_rows, uint16_t* v_rows,
+                          const int32_t* block_table, int bt_stride, const int32_t* ctx_lens,
+                          const int32_t* cu_q_lens, int batch, int max_q_len, int num_kv_heads, int head_dim,
+                          int num_pages, int total_q, hipStream_t stream);
 
 hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32_t* cu_q_lens,
                        void* workspace, const WsLayout& lay, hipStream_t stream);

@@ -110,6 +110,21 @@ def test_kv_append_host_validation():
     assert f(None, ctypes.byref(d), FAKE, FAKE, FAKE, FAKE, None) == INVALID
 
 
+@pytest.mark.parametrize("fn", ["pearl_kv_pack", "pearl_kv_unpack"])
+def test_kv_transfer_host_validation(fn):
+    f = getattr(pa.load(), fn)
+    s, d = shape(), desc()
+    assert f(ctypes.byref(s), ctypes.byref(d), FAKE, FAKE, None, None) == INVALID
+    assert f(ctypes.byref(s), ctypes.byref(d), FAKE, FAKE + 8, FAKE, None) == INVALID   # misaligned
+    assert f(ctypes.byref(shape(d=80)), ctypes.byref(d), FAKE, FAKE, FAKE, None) == UNSUPPORTED
+    assert f(ctypes.byref(s), ctypes.byref(desc(batch=0)), FAKE, FAKE, FAKE, None) == INVALID
+    assert f(None, ctypes.byref(d), FAKE, FAKE, FAKE, None) == INVALID
+    assert f(ctypes.byref(s), ctypes.byref(desc(max_q=1 << 22, total=1 << 22, cu=FAKE, max_kv=1 << 23,
+                                                stride=1 << 19)), FAKE, FAKE, FAKE, None) == UNSUPPORTED
+    # nothing to move: succeeds without touching the GPU
+    assert f(ctypes.byref(s), ctypes.byref(desc(total=0, cu=FAKE, max_q=0)), FAKE, FAKE, FAKE, None) == 0
+
+
 def test_python_layer_refuses_cpu_tensors():
     import torch
     q = torch.zeros(2, 4, 64, dtype=torch.bfloat16)
