@@ -202,6 +202,16 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
 
 }  // namespace
 
+void clear_error() { g_err[0] = 0; }
+
+pearl_status set_error(pearl_status st, const char* fmt, ...) {
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(g_err, sizeof(g_err), fmt, ap);
+  va_end(ap);
+  return st;
+}
+
 int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu) {
   // Aim for about 16 decode items per compute unit when every sequence is as long as the bound;
   // a split never holds fewer than 16 pages (one page pair for each of the 8 waves), and its size

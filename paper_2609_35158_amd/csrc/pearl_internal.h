@@ -6,7 +6,13 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "../../include/pearl_attn.h"
+
 namespace pearl {
+
+// Thread-local detail message returned by pearl_last_error() (defined in api.cpp).
+void clear_error();
+pearl_status set_error(pearl_status st, const char* fmt, ...);
 
 constexpr int kPage = 16;            // tokens per KV page
 constexpr int kThreads = 512;        // threads per attention workgroup (8 waves of 64)
