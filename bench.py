@@ -13,8 +13,8 @@ The same line carries:
   cpu_baseline  the CPU oracle (numpy float64) timed on this host on a bounded sample;
   secondary     prefill-append TFLOP/s (Qwen3-8B shape), Qwen3-30B-A3B-shaped decode at batch
                 256/128/32, the colocated mixed batch, kv_append GB/s, KV transfer pack/unpack
-                GB/s, and a decode/prefill interference sweep (one mixed launch vs decode alone
-                as prefill chunks grow).
+                GB/s, a decode/prefill interference sweep (one mixed launch vs decode alone
+                as prefill chunks grow), and the PD decision engine calibrated from the kernels.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-secondary] [--no-cpu]
 """
@@ -307,6 +307,112 @@ def kv_transfer(torch, pa, workloads, steps, warmup):
 
 
 # ------------------------------------------------------------------------------------------------
+# PD decision engine calibrated from the kernels
+# ------------------------------------------------------------------------------------------------
+
+# Public architecture facts of the two models (layers, kv-heads, head_dim, parameters).
+MODELS = {
+    "qwen3-8b": {"layers": 36, "num_kv_heads": 8, "head_dim": 128, "params_total": 8.2e9, "params_active": 8.2e9},
+    "qwen3-30b-a3b": {"layers": 48, "num_kv_heads": 4, "head_dim": 128, "params_total": 30.5e9,
+                      "params_active": 3.3e9},
+}
+# Workload profile and platform inputs the kernels cannot measure (stated, not fitted): rollout
+# batch 64 with tensor parallelism 2 per worker (the paper's evaluation setup), 800 Gb/s between
+# pools, 288 GB HBM per GPU.
+PD_INPUTS = {"B": 64.0, "S": 40.0, "dL": 600.0, "r": 300.0, "T_env": 120.0,
+             "BW": 100e9, "u_max": 1.0, "tp": 2, "hbm_per_gpu": 288e9, "mean_traj_tokens": 16384.0}
+# Two workload profiles: many environment bubbles and cheap prefill/decode switching, versus few
+# bubbles and costly switching (the regimes in which the paper finds colocation, respectively
+# disaggregation, preferable).
+PD_PROFILES = {"bubbly": {"theta": 0.3, "T_over": 0.05}, "interfering": {"theta": 0.05, "T_over": 1.0}}
+
+
+def pd_engine(torch, pa, workloads, steps, warmup):
+    """Calibrate the makespan-model costs from this GPU's kernels (decode attention time vs batch
+    -> A_attn, b_attn per layer; prefill attention time vs new tokens -> per-token time), refit
+    with the library's own telemetry refits, scale to whole models, then run the decision engine
+    over rollout-worker budgets and time one decision."""
+    import numpy as np
+    from paper_2609_35158_amd import pd
+
+    def attn_ms(case, mode):
+        st, out = make_step(torch, pa, case, mode)
+        _, ms = run_timed(torch, pa, lambda hook: st(hook, append=False), steps, warmup)
+        del st, out
+        return ms
+
+    cal = {}
+    for model, gen, sizes in (("qwen3-8b", lambda: workloads.qwen3_8b_decode("cuda"), (8, 16, 32, 64)),
+                              ("qwen3-30b-a3b", lambda: workloads.qwen3_30b_decode("cuda", batch=256),
+                               (32, 64, 128, 256))):
+        base = gen()
+        fill, _ = make_step(torch, pa, base, "decode")
+        fill(lambda: None, attention=False)
+        xs, ys, ctx_mean = [], [], []
+        for n in sizes:
+            sub = workloads.sub_batch(base, list(range(n)))
+            xs.append(float(n))
+            ys.append(attn_ms(sub, "decode") * 1e-3)
+            ctx_mean.append(float(sub.kv_lens.mean()))
+        A_attn, b_attn = pd.fit_decode_cost(xs, ys)
+        cal[model] = {"decode_batch": xs, "decode_s": [round(y, 8) for y in ys], "A_attn_s": A_attn,
+                      "b_attn_s": b_attn, "mean_context": float(np.mean(ctx_mean)),
+                      "decode_GBps": round(attn_bytes(base) / (ys[-1]) / 1e9, 1)}
+        del base, fill
+        torch.cuda.empty_cache()
+    pre = workloads.qwen3_8b_prefill_append("cuda")
+    fill, _ = make_step(torch, pa, pre, "prefill")
+    fill(lambda: None, attention=False)
+    toks, secs, flops, tfl = [], [], 0.0, []
+    for n in (2, 4, 8, 16):
+        sub = workloads.sub_batch(pre, list(range(n)))
+        t = attn_ms(sub, "prefill") * 1e-3
+        toks.append(float(sub.total_q))
+        secs.append(t)
+        tfl.append(attn_flops(sub) / t / 1e12)
+    t_attn_tok = pd.fit_prefill_cost(toks, secs)
+    mfma_tflops = max(tfl)
+    del pre, fill
+    torch.cuda.empty_cache()
+
+    I = PD_INPUTS
+    out_models = []
+    for (model, m), (prof, pv) in [(mm, pp) for mm in MODELS.items() for pp in PD_PROFILES.items()]:
+        c = cal[model]
+        tp = I["tp"]
+        hbm_rate = c["decode_GBps"] * 1e9                      # measured streaming rate of this GPU
+        weight_s = m["params_total"] * 2 / tp / hbm_rate          # bf16 weights read once per iteration
+        K = 2 * m["layers"] * m["num_kv_heads"] * m["head_dim"] * 2
+        p = dict(B=I["B"], S=I["S"], dL=I["dL"], r=I["r"], theta=pv["theta"], T_over=pv["T_over"],
+                 T_env=I["T_env"], BW=I["BW"], u_max=I["u_max"],
+                 A=weight_s + m["layers"] * c["A_attn_s"],
+                 b=m["layers"] * c["b_attn_s"] / tp,
+                 t_prefill=2 * m["params_active"] / (tp * mfma_tflops * 1e12) + m["layers"] * t_attn_tok / tp,
+                 K=float(K), K_seq=K * I["mean_traj_tokens"],
+                 H_max=tp * I["hbm_per_gpu"] * 0.9 - m["params_total"] * 2)
+        table = []
+        for n in range(1, 9):
+            best, t_coloc, best_dis = pd.best_config(p, n)
+            table.append({"workers": n, "mode": "dis" if best[0] == pd.DIS else "coloc",
+                          "N_P": best[1], "N_D": best[2], "makespan_s": round(best[4], 3),
+                          "coloc_s": round(t_coloc, 3),
+                          "best_dis_s": None if best_dis is None else round(best_dis[4], 3)})
+        reps = 20000
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            pd.decide(p, 8, (pd.DIS, 2, 6), 0.1, 0.03)
+        us = (time.perf_counter() - t0) / reps * 1e6
+        e = {"model": model, "profile": prof, "params": {k: (round(v, 9) if isinstance(v, float) else v) for k, v in p.items()},
+             "decisions": table, "decide_us_per_call_incl_ctypes": round(us, 2)}
+        log("bench:   pd-engine %s %s: %s" % (model, prof, " ".join("%d:%s%s" % (t["workers"], t["mode"],
+            "(%d/%d)" % (t["N_P"], t["N_D"]) if t["mode"] == "dis" else "") for t in table)))
+        out_models.append(e)
+    return {"workload": "pd-engine", "mode": "host", "calibration": cal,
+            "prefill_attn_s_per_token_layer": t_attn_tok, "prefill_mfma_tflops": round(mfma_tflops, 1),
+            "inputs": I, "models": out_models}
+
+
+# ------------------------------------------------------------------------------------------------
 # CPU oracle baseline on a bounded sample
 # ------------------------------------------------------------------------------------------------
 
@@ -523,6 +629,9 @@ def main():
         if not only or "kv-transfer" in only:
             log("bench: secondary kv-transfer")
             sec.extend(kv_transfer(torch, pa, workloads, args.steps, args.warmup))
+        if not only or "pd-engine" in only:
+            log("bench: secondary pd-engine")
+            sec.append(pd_engine(torch, pa, workloads, max(5, args.steps // 2), args.warmup))
         if not only or "pd-interference" in only:
             log("bench: secondary pd-interference")
             sec.append(pd_interference(torch, pa, workloads, max(5, args.steps // 2), args.warmup))
