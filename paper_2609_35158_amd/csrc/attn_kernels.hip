@@ -111,7 +111,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     int2* __restrict__ entries, int4* __restrict__ pre_jobs) {
   __shared__ int s_err, s_tiles, s_max_full, s_split_keys;
   __shared__ unsigned long long s_pre_keys, s_dec_keys;
-  __shared__ int s_scan[3][kPlanThreads];
+  __shared__ int s_wave[3][kPlanThreads / 64];
   __shared__ int s_carry[3];
   const int tid = threadIdx.x;
   const int T = p.tokens_per_tile;
@@ -202,21 +202,29 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         }
       }
     }
+    // exclusive scan: wave-level inclusive scans by shuffles, then the totals of earlier waves
+    const int lane = tid & 63, wv = tid >> 6;
+    int incl[3] = {cnt[0], cnt[1], cnt[2]};
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+#pragma unroll
+      for (int c = 0; c < 3; ++c) {
+        const int v = __shfl_up(incl[c], off);
+        if (lane >= off) incl[c] += v;
+      }
+    }
+    if (lane == 63) {
+#pragma unroll
+      for (int c = 0; c < 3; ++c) s_wave[c][wv] = incl[c];
+    }
+    __syncthreads();
     int excl[3];
 #pragma unroll
-    for (int c = 0; c < 3; ++c) s_scan[c][tid] = cnt[c];
-    __syncthreads();
-    for (int off = 1; off < kPlanThreads; off <<= 1) {
-      int add[3];
-#pragma unroll
-      for (int c = 0; c < 3; ++c) add[c] = tid >= off ? s_scan[c][tid - off] : 0;
-      __syncthreads();
-#pragma unroll
-      for (int c = 0; c < 3; ++c) s_scan[c][tid] += add[c];
-      __syncthreads();
+    for (int c = 0; c < 3; ++c) {
+      int before = s_carry[c];
+      for (int k = 0; k < wv; ++k) before += s_wave[c][k];
+      excl[c] = before + incl[c] - cnt[c];
     }
-#pragma unroll
-    for (int c = 0; c < 3; ++c) excl[c] = s_scan[c][tid] - cnt[c] + s_carry[c];
     if (b < p.batch) {
       seqinfo[b] = SeqInfo{q_start, q_len, ctx, kind | (cnt[1] << 4)};
       split_base[b] = excl[1];
@@ -805,17 +813,39 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a, int batch) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
   constexpr int PER = D / 64;
+  constexpr int U = 8;                              // splits whose o~ loads are in flight together
   float acc[PER];
 #pragma unroll
   for (int i = 0; i < PER; ++i) acc[i] = 0.f;
   float L = 0.f;
-  for (int s = 0; s < ns; ++s) {
-    const size_t pidx = (base + s) * H_q + h;
-    const float f = fexp2(a.part_ml[2 * pidx] - M);
-    L += f * a.part_ml[2 * pidx + 1];
+  for (int s0 = 0; s0 < ns; s0 += 64) {
+    const int cnt = min(64, ns - s0);
+    // lane j computes split s0 + j's weight 2^(m - M) and its share of the sum
+    float f = 0.f;
+    if (lane < cnt) {
+      const size_t pidx = (base + s0 + lane) * H_q + h;
+      f = fexp2(a.part_ml[2 * pidx] - M);
+      L += f * a.part_ml[2 * pidx + 1];
+    }
+    for (int j = 0; j < cnt; j += U) {
+      float v[U][PER], fj[U];
 #pragma unroll
-    for (int i = 0; i < PER; ++i) acc[i] += f * a.part_o[pidx * D + lane * PER + i];
+      for (int u = 0; u < U; ++u) {
+        const int jj = min(j + u, cnt - 1);       // past the end: reload the last split, weight 0
+        const float w = __shfl(f, jj);
+        fj[u] = j + u < cnt ? w : 0.f;
+        const size_t pidx = (base + s0 + jj) * H_q + h;
+#pragma unroll
+        for (int i = 0; i < PER; ++i) v[u][i] = a.part_o[pidx * D + lane * PER + i];
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < PER; ++i) acc[i] += fj[u] * v[u][i];
+    }
   }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) L += __shfl_xor(L, off);
   const float inv = 1.0f / L;
   uint16_t* orow = a.out + ((size_t)si.q_start * H_q + h) * D + lane * PER;
 #pragma unroll
