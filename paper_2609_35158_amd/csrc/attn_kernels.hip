@@ -63,6 +63,22 @@ __device__ __forceinline__ bf16x8 concat_tr(i16x4 a, i16x4 b) {
   return __builtin_bit_cast(bf16x8, v);
 }
 
+// Combine x with the value held by lane l ^ 32, using v_permlane32_swap (one VALU instruction,
+// no LDS round trip).  With both operands x, the swap returns r0 = (x[l] for l < 32, x[l-32]
+// otherwise) and r1 = (x[l+32] for l < 32, x[l] otherwise); both halves then combine the same
+// two values in the same order, so the results are bit-identical across the pair.
+__device__ __forceinline__ float xor32_max(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return fmaxf(__builtin_bit_cast(float, (unsigned)r[0]), __builtin_bit_cast(float, (unsigned)r[1]));
+}
+
+__device__ __forceinline__ float xor32_add(float x) {
+  const unsigned u = __builtin_bit_cast(unsigned, x);
+  const auto r = __builtin_amdgcn_permlane32_swap(u, u, false, false);
+  return __builtin_bit_cast(float, (unsigned)r[0]) + __builtin_bit_cast(float, (unsigned)r[1]);
+}
+
 // The block table is read-only for the whole kernel; reading it through the constant address
 // space lets the compiler use scalar loads (counted by lgkmcnt, not vmcnt) for these uniform reads.
 typedef const __attribute__((address_space(4))) int32_t* ConstI32Ptr;
@@ -344,14 +360,24 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   auto store_stage = [&](int step, int buf, const Stage& S) {
     char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
     char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
-    const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+    if ((step + 1) * kKeysPerStage <= kv_needed) {   // every row of the stage is a needed key
 #pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int cidx = threadIdx.x + i * kThreads;
-      const int kk = cidx / CPR, dc = cidx - kk * CPR;
-      const bool ok = step * kKeysPerStage + kk < kv_needed;
-      *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = ok ? S.k[i] : zero;
-      *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = ok ? S.v[i] : zero;
+      for (int i = 0; i < NCH; ++i) {
+        const int cidx = threadIdx.x + i * kThreads;
+        const int kk = cidx / CPR, dc = cidx - kk * CPR;
+        *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = S.k[i];
+        *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = S.v[i];
+      }
+    } else {
+      const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
+#pragma unroll
+      for (int i = 0; i < NCH; ++i) {
+        const int cidx = threadIdx.x + i * kThreads;
+        const int kk = cidx / CPR, dc = cidx - kk * CPR;
+        const bool ok = step * kKeysPerStage + kk < kv_needed;
+        *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = ok ? S.k[i] : zero;
+        *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = ok ? S.v[i] : zero;
+      }
     }
   };
   auto compute = [&](int step, int buf) {
@@ -370,8 +396,10 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
           s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
         }
       }
-      // causal mask (only on steps that reach past some row's last visible key)
+      // causal mask (only on steps that reach past some row's last visible key); the empty asm
+      // keeps this a real branch: the compiler would otherwise evaluate the mask on every step
       if (k0 + kKeysPerStage - 1 > wave_min_limit) {
+        __asm__ volatile("" ::);
 #pragma unroll
         for (int st = 0; st < 2; ++st)
 #pragma unroll
@@ -386,7 +414,7 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
       for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
 #pragma unroll
       for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      mx = xor32_max(mx);
       // the row maximum only moves when this tile exceeds it; the O rescale is skipped when no
       // row of the wave moved (the largest weight of a row is then exactly 1 in bf16)
       const bool grow = mx * c > m_run;
@@ -404,6 +432,7 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
         }
       l_run = l_run * alpha + psum;
       if (__ballot(grow)) {
+        __asm__ volatile("" ::);                   // a real branch, not a speculated rescale
 #pragma unroll
         for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
@@ -450,7 +479,7 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   }
 
   // epilogue: combine the two half-row sums; a split item stores its fp32 partial state
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = xor32_add(l_run);
   if (row_ok && n_split > 1) {
     const size_t prow = (size_t)(e * H_kv + g) * kRowsPerTile + rho;
     float* po = a.part_pre_o + prow * D;
