@@ -286,7 +286,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 // A split item (entry e, code = tile | split << 16) covers only its key range and writes the
 // unnormalised (o~, m, l) of its rows to partial slot e * H_kv + g for the prefill merge.
 // ------------------------------------------------------------------------------------------------
-template <int D>
+// kHoistV: read the first dim block's V^T operands before the softmax (needs 16 more VGPRs; used
+// where the kernel has them to spare).
+template <int D, bool kHoistV>
 __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
                                              char* smem) {
   constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
@@ -396,6 +398,21 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
           s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
         }
       }
+      // with kHoistV the V^T operands of the first 32-dim block are read now, so their LDS
+      // latency hides behind the softmax instead of stalling the first P.V products
+      const int gi = lane >> 4, jl = lane & 15;
+      const int krow = 4 * (gi >> 1) + (jl >> 2);
+      const int dcol = 16 * (gi & 1) + 4 * (jl & 3);
+      bf16x8 vfirst[2][2];
+      if constexpr (kHoistV) {
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int kk = 0; kk < 2; ++kk) {
+            const int off = (32 * st + 16 * kk + krow) * VS + dcol * 2;
+            vfirst[st][kk] = concat_tr(lds_read_tr(vb_, off), lds_read_tr(vb_, off + 8 * VS));
+          }
+      }
       // causal mask (only on steps that reach past some row's last visible key); the empty asm
       // keeps this a real branch: the compiler would otherwise evaluate the mask on every step
       if (k0 + kKeysPerStage - 1 > wave_min_limit) {
@@ -440,22 +457,21 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
       }
       m_run = m_new;
       // O^T += V^T P^T
-      {
-        const int gi = lane >> 4, j = lane & 15;
-        const int krow = 4 * (gi >> 1) + (j >> 2);
-        const int dcol = 16 * (gi & 1) + 4 * (j & 3);
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+      for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-          for (int st = 0; st < 2; ++st)
+        for (int st = 0; st < 2; ++st)
 #pragma unroll
-            for (int kk = 0; kk < 2; ++kk) {
+          for (int kk = 0; kk < 2; ++kk) {
+            bf16x8 vop;
+            if (kHoistV && mb == 0) {
+              vop = vfirst[st][kk];
+            } else {
               const int off = (32 * st + 16 * kk + krow) * VS + (32 * mb + dcol) * 2;
-              const i16x4 v0 = lds_read_tr(vb_, off);
-              const i16x4 v1 = lds_read_tr(vb_, off + 8 * VS);
-              oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(concat_tr(v0, v1), pop[st][kk], oacc[mb], 0, 0, 0);
+              vop = concat_tr(lds_read_tr(vb_, off), lds_read_tr(vb_, off + 8 * VS));
             }
-      }
+            oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[st][kk], oacc[mb], 0, 0, 0);
+          }
   };
 
   Stage sA, sB;
@@ -806,7 +822,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
       if constexpr ((kKinds & 1) != 0) {
         static_assert(NW == kWaves, "prefill tiles use 8 waves");
         const int2 en = a.entries[e];
-        prefill_tile<D>(a, e, en.x, en.y, g, split_keys, smem);
+        prefill_tile<D, kKinds == 1>(a, e, en.x, en.y, g, split_keys, smem);
       }
     } else {
       if constexpr ((kKinds & 2) != 0) {
