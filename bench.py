@@ -407,7 +407,31 @@ def pd_engine(torch, pa, workloads, steps, warmup):
         log("bench:   pd-engine %s %s: %s" % (model, prof, " ".join("%d:%s%s" % (t["workers"], t["mode"],
             "(%d/%d)" % (t["N_P"], t["N_D"]) if t["mode"] == "dis" else "") for t in table)))
         out_models.append(e)
-    return {"workload": "pd-engine", "mode": "host", "calibration": cal,
+    # minimal-change plan over a 64-slot worker table and the toggle decision (host latency,
+    # including the ctypes call)
+    trng = np.random.default_rng(11)
+    cur = [int(x) for x in trng.integers(0, 4, size=64)]
+    target = [bool(x) for x in trng.integers(0, 2, size=64)]
+    m_act = sum(target)
+    counts = (m_act // 4, m_act // 2, m_act - m_act // 4 - m_act // 2)
+    reps = 20000
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        new_role, d_worker, d_role = pd.plan_min_change(cur, target, *counts)
+    plan_us = (time.perf_counter() - t0) / reps * 1e6
+    p_last = out_models[-1]["params"]
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        enable, T_ded, T_full = pd.toggle_decide(p_last, 4, 8, 40.0, 30.0)
+    gate_us = (time.perf_counter() - t0) / reps * 1e6
+    plan = {"slots": 64, "active_after": m_act, "target_counts": counts, "d_worker": d_worker, "d_role": d_role,
+            "plan_us_per_call_incl_ctypes": round(plan_us, 2),
+            "toggle_decide_us_per_call_incl_ctypes": round(gate_us, 2),
+            "toggle_example": {"n_ded": 4, "n_overlap": 8, "R": 40.0, "T_toggle_s": 30.0, "enable": enable,
+                               "T_ded_s": round(T_ded, 3), "T_full_s": round(T_full, 3)}}
+    log("bench:   pd-engine plan %.2f us (64 slots, %d membership + %d role changes), toggle decision %.2f us"
+        % (plan_us, d_worker, d_role, gate_us))
+    return {"workload": "pd-engine", "mode": "host", "calibration": cal, "plan_and_gate": plan,
             "prefill_attn_s_per_token_layer": t_attn_tok, "prefill_mfma_tflops": round(mfma_tflops, 1),
             "inputs": I, "models": out_models}
 
@@ -433,36 +457,47 @@ def compact_pool(torch, case, seqs):
 
 
 def cpu_baseline(torch, case, out, budget_s):
-    """Time the oracle (single BLAS thread) decoding whole sequences of the same workload until
-    `budget_s` seconds have passed; also report the parity of the GPU output on those sequences."""
+    """Time the oracle (single BLAS thread) decoding whole sequences of the same workload, in a
+    random order, passing over the batch again until `budget_s` seconds of oracle time have
+    been spent; the first pass also gives the parity of the GPU output on every sequence it
+    reaches."""
     import numpy as np
     from threadpoolctl import threadpool_limits
     import oracle
     as_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
     q_bits = as_bits(case.q)
     out_bits = as_bits(out)
-    done, t_total = 0, 0.0
+    done, t_total, passes = 0, 0.0, 0
+    keys = 0
     errs = []
+    pools = {}
     rng = np.random.default_rng(123)
     order = rng.permutation(case.batch)
     with threadpool_limits(limits=1):
-        for b in order:
-            kp, vp, sbt = compact_pool(torch, case, [int(b)])
-            t0 = time.perf_counter()
-            o, _ = oracle.attention(q_bits[b:b + 1], kp, vp, sbt, case.ctx_lens[b:b + 1], None, case.scale)
-            t_total += time.perf_counter() - t0
-            done += 1
-            errs.append(oracle.compare(out_bits[b:b + 1], o))
-            if t_total >= budget_s:
-                break
-    keys = int(case.kv_lens[order[:done]].sum())
+        while t_total < budget_s:
+            for b in order:
+                b = int(b)
+                if b not in pools:
+                    pools[b] = compact_pool(torch, case, [b])
+                kp, vp, sbt = pools[b]
+                t0 = time.perf_counter()
+                o, _ = oracle.attention(q_bits[b:b + 1], kp, vp, sbt, case.ctx_lens[b:b + 1], None, case.scale)
+                t_total += time.perf_counter() - t0
+                done += 1
+                keys += int(case.kv_lens[b])
+                if passes == 0:
+                    errs.append(oracle.compare(out_bits[b:b + 1], o))
+                if t_total >= budget_s:
+                    break
+            passes += 1
     return {
         "value": done / t_total, "unit": "tok/s", "cores": 1, "kind": "oracle",
-        "sample": "%d of %d sequences of the same decode batch (%d keys, all %d q-heads), numpy float64, "
-                  "1 BLAS thread, %.1f s" % (done, case.batch, keys, case.num_q_heads, t_total),
+        "sample": "%d sequence decodes (%d passes over the %d-sequence decode batch in random order, %d keys "
+                  "attended, all %d q-heads), numpy float64, 1 BLAS thread, %.1f s"
+                  % (done, passes, case.batch, keys, case.num_q_heads, t_total),
         "cpu": cpu_model(),
     }, {
-        "sequences": done,
+        "sequences": len(errs),
         "max_abs": max(e["max_abs"] for e in errs), "mean_abs": float(np.mean([e["mean_abs"] for e in errs])),
     }
 

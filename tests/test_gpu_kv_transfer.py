@@ -150,3 +150,42 @@ def test_full_context_transfer_fullsize():
         L = int(lens[b])
         flat = lambda x: x.transpose(0, 2, 1, 3).reshape(npg * PAGE, x.shape[1], x.shape[3])[:L]
         assert np.array_equal(flat(kb), flat(ka)) and np.array_equal(flat(vb), flat(va)), "sequence %d" % b
+
+
+def test_out_of_range_pages_pack_zeros_and_unpack_skips():
+    """Documented behaviour for block-table entries outside [0, num_pages): a pack writes zero rows
+    for them and an unpack leaves the pools untouched for them (no access happens: the kernel
+    checks the id before addressing the pool)."""
+    say("case: kv transfer with out-of-range page ids")
+    lens = np.array([40, 20])
+    case = workloads.build_case("xfer-oob", 51, 4, 4, 64, lens, np.zeros(2, np.int64), device="cuda")
+    bt = case.block_table.cpu().numpy().copy()
+    bt[0, 1] = -1                       # positions 16..31 of sequence 0
+    bt[1, 0] = case.num_pages           # positions 0..15 of sequence 1
+    bt_d = _dev(bt)
+    cu = np.array([0, 40, 60], np.int32)
+    zeros = _dev(np.zeros(2, np.int64))
+    buf = pa.kv_pack(case.k_pool, case.v_pool, bt_d, zeros, _dev(cu), 60, 40, 40)
+    torch.cuda.synchronize()
+    got = bits(buf)
+    ref_bt = case.block_table.cpu().numpy()
+    ref = oracle.kv_pack(bits(case.k_pool), bits(case.v_pool), ref_bt, np.zeros(2, np.int64), cu)
+    bad_rows = list(range(16, 32)) + list(range(40, 56))
+    good_rows = [r for r in range(60) if r not in bad_rows]
+    assert np.all(got[:, bad_rows] == 0)
+    assert np.array_equal(got[:, good_rows], ref[:, good_rows])
+    k0, v0 = bits(case.k_pool), bits(case.v_pool)
+    pa.kv_unpack(buf.flip(-1).contiguous(), case.k_pool, case.v_pool, bt_d, zeros, _dev(cu), 40, 40)
+    torch.cuda.synchronize()
+    # the oracle takes the valid table; only rows whose id is valid in `bt` are compared, and the
+    # pages behind the two invalid ids must be unchanged
+    kr, vr = oracle.kv_unpack(k0, v0, bits(buf.flip(-1).contiguous()), ref_bt, np.zeros(2, np.int64), cu)
+    kg, vg = bits(case.k_pool), bits(case.v_pool)
+    for pg in (int(ref_bt[0, 1]), int(ref_bt[1, 0])):
+        assert np.array_equal(kg[pg], k0[pg]) and np.array_equal(vg[pg], v0[pg])
+    for b, L in ((0, 40), (1, 20)):
+        for p in range(L):
+            if bt[b, p // 16] < 0 or bt[b, p // 16] >= case.num_pages:
+                continue
+            pg, sl = bt[b, p // 16], p % 16
+            assert np.array_equal(kg[pg, :, sl], kr[pg, :, sl]) and np.array_equal(vg[pg, :, sl], vr[pg, :, sl])
