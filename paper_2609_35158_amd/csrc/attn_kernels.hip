@@ -346,17 +346,24 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   const ConstI32Ptr bt_c = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
   const int last_pidx = (kv_needed - 1) / kPage;
   struct Stage { u32x4 k[NCH], v[NCH]; };
+  // byte offset of this thread's chunk i inside its (page, kv-head) block: constant over stages
+  // (stages start on page boundaries); the block's base is uniform per wave, so each load is a
+  // scalar base plus one 32-bit vector offset
+  uint32_t toff[NCH];
+#pragma unroll
+  for (int i = 0; i < NCH; ++i) {
+    const int cidx = threadIdx.x + i * kThreads;
+    const int kk = cidx / CPR, dc = cidx - kk * CPR;
+    toff[i] = (uint32_t)(((kk % kPage) * D + dc * 8) * 2);
+  }
   auto load_stage = [&](int step, Stage& S) {
 #pragma unroll
     for (int i = 0; i < NCH; ++i) {
-      const int cidx = threadIdx.x + i * kThreads;
-      const int kk = cidx / CPR, dc = cidx - kk * CPR;
-      const int j = step * kKeysPerStage + kk;
       const int pidx = min(step * (kKeysPerStage / kPage) + (64 * w + kThreads * i) / (kPage * CPR), last_pidx);
       const int page = clamp_page(bt_c[pidx], a.num_pages);
-      const size_t off = ((size_t)page * H_kv + g) * head_stride + (size_t)(j % kPage) * D + dc * 8;
-      S.k[i] = ld16(a.k_pool + off);
-      S.v[i] = ld16(a.v_pool + off);
+      const size_t base = (((size_t)page * H_kv + g) * head_stride) * 2;
+      S.k[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(a.k_pool) + base + toff[i]);
+      S.v[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(a.v_pool) + base + toff[i]);
     }
   };
   auto store_stage = [&](int step, int buf, const Stage& S) {

@@ -377,3 +377,28 @@ def test_prefill_key_splits_long_context_sampled():
     toks = [0, 1, 31, 32, 100, 200, 254, 255]
     o_ref, l_ref = oracle_sampled(case, [0], {0: toks})
     assert_close(bits(out)[toks], o_ref[0][toks], lse.cpu().numpy()[toks], l_ref[0][toks], what="long split")
+
+
+def test_batches_larger_than_one_planner_chunk():
+    """More sequences than the planner's 1024 threads: the block scan carries offsets from one
+    chunk of sequences to the next (decode: 1500 sequences; mixed: 1100 sequences with ragged
+    chunks and decodes)."""
+    say("case: 1500-sequence decode and 1100-sequence mixed batch")
+    rng = np.random.default_rng(77)
+    ctx = rng.integers(0, 90, size=1500, endpoint=True)
+    case = workloads.build_case("big-batch-dec", 7701, 8, 2, 64, ctx, np.ones(1500, np.int64), device="cuda")
+    kr, vr = _append_and_check(case)
+    o_ref, l_ref = oracle_full(case, kr, vr)
+    out, lse = gpu_attend(case, "decode")
+    torch.cuda.synchronize()
+    assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="1500-sequence decode")
+    ctx = rng.integers(0, 60, size=1100, endpoint=True)
+    ql = np.where(rng.random(1100) < 0.5, 1, rng.integers(0, 9, size=1100, endpoint=True))
+    case = workloads.build_case("big-batch-mixed", 7702, 8, 2, 64, ctx, ql, device="cuda")
+    kr, vr = _append_and_check(case)
+    o_ref, l_ref = oracle_full(case, kr, vr)
+    for mode in ("mixed", "prefill"):
+        out, lse = gpu_attend(case, mode)
+        torch.cuda.synchronize()
+        m = np.isfinite(o_ref).all(axis=(1, 2))
+        assert_close(bits(out)[m], o_ref[m], lse.cpu().numpy()[m], l_ref[m], what="1100-sequence " + mode)
