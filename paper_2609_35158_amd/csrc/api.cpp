@@ -142,6 +142,10 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   const int64_t total_rows = (int64_t)q->total_q * s->num_q_heads * s->head_dim;
   if (total_rows > INT32_MAX * int64_t(8)) return fail(PEARL_ERR_UNSUPPORTED, "q/out too large");
   Plan pl = make_plan(s, q, mode);
+  // the device keeps entry and item counts in int32
+  if ((pl.lay.max_pre + pl.lay.max_dec) * (int64_t)s->num_kv_heads > INT32_MAX)
+    return fail(PEARL_ERR_UNSUPPORTED, "work list bound (%lld entries x %d kv-heads) exceeds int32",
+                (long long)(pl.lay.max_pre + pl.lay.max_dec), s->num_kv_heads);
   if (ws_bytes < pl.lay.total)
     return fail(PEARL_ERR_WORKSPACE, "workspace_bytes %zu < required %zu", ws_bytes, pl.lay.total);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -252,7 +256,6 @@ WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_head
   l.part_pre_o = off; off = align256(off + sizeof(float) * (size_t)l.pre_slots * kRowsPerTile * head_dim);
   l.part_pre_ml = off; off = align256(off + sizeof(float) * 2 * (size_t)l.pre_slots * kRowsPerTile);
   l.total = off;
-  (void)num_kv_heads;
   return l;
 }
 

@@ -29,6 +29,9 @@
 
 #include <math.h>
 
+#include <atomic>
+#include <mutex>
+
 namespace pearl {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
@@ -955,7 +958,10 @@ __global__ __launch_bounds__(256) void merge_prefill_kernel(AttnArgs a) {
 // host launchers
 // ------------------------------------------------------------------------------------------------
 namespace {
+// Launch parameters per device (compute units, occupancy per kernel), queried on the first call
+// that runs on the device.  Initialisation is guarded so concurrent first calls are safe.
 struct DevCache {
+  std::atomic<int> ready{0};
   int num_cu = 0;
   int occ[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};   // [D == 128][kinds]
 };
@@ -966,19 +972,35 @@ int occupancy_of() {
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, attn_kernel<D, K>, KernelCfg<D, K>::NT, 0) != hipSuccess || o < 1) o = 1;
   return o;
 }
-DevCache g_cache[64];
 
-DevCache& dev_cache() {
+void fill_cache(DevCache& c, int dev) {
+  hipDeviceProp_t prop;
+  int ncu = 256;
+  if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0) ncu = prop.multiProcessorCount;
+  c.occ[0][1] = occupancy_of<64, 1>(); c.occ[0][2] = occupancy_of<64, 2>(); c.occ[0][3] = occupancy_of<64, 3>();
+  c.occ[1][1] = occupancy_of<128, 1>(); c.occ[1][2] = occupancy_of<128, 2>(); c.occ[1][3] = occupancy_of<128, 3>();
+  c.num_cu = ncu;
+}
+
+constexpr int kCachedDevices = 64;
+DevCache g_cache[kCachedDevices];
+std::mutex g_cache_mutex;
+
+const DevCache& dev_cache() {
   int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0) dev = 0;
+  if (dev >= kCachedDevices) {                   // beyond the cache: query every time
+    thread_local DevCache t;
+    fill_cache(t, dev);
+    return t;
+  }
   DevCache& c = g_cache[dev];
-  if (c.num_cu == 0) {
-    hipDeviceProp_t prop;
-    int ncu = 256;
-    if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0) ncu = prop.multiProcessorCount;
-    c.occ[0][1] = occupancy_of<64, 1>(); c.occ[0][2] = occupancy_of<64, 2>(); c.occ[0][3] = occupancy_of<64, 3>();
-    c.occ[1][1] = occupancy_of<128, 1>(); c.occ[1][2] = occupancy_of<128, 2>(); c.occ[1][3] = occupancy_of<128, 3>();
-    c.num_cu = ncu;
+  if (!c.ready.load(std::memory_order_acquire)) {
+    std::lock_guard<std::mutex> lock(g_cache_mutex);
+    if (!c.ready.load(std::memory_order_relaxed)) {
+      fill_cache(c, dev);
+      c.ready.store(1, std::memory_order_release);
+    }
   }
   return c;
 }
@@ -1000,7 +1022,7 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t 
                             hipStream_t stream) {
   if (max_items <= 0) return hipSuccess;
   if (kinds < 1 || kinds > 3) return hipErrorInvalidValue;
-  DevCache& c = dev_cache();
+  const DevCache& c = dev_cache();
   const int occ = c.occ[head_dim == 128 ? 1 : 0][kinds];
   int64_t grid = (int64_t)c.num_cu * occ;
   if (grid > max_items) grid = max_items;
