@@ -119,6 +119,7 @@ Plan make_plan(const pearl_kv_shape* s, const pearl_seq_desc* q, int mode) {
   p.max_dec = pl.lay.max_dec;
   p.pre_slots = mode == kModeDecode ? 0 : pl.lay.pre_slots;
   p.pre_jobs_cap = mode == kModeDecode ? 0 : pl.lay.pre_jobs_cap;
+  p.mixed_grid = mode == kModeMixed ? attention_grid(s->head_dim, 3) : 0;
   return pl;
 }
 

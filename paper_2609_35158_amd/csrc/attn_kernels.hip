@@ -128,7 +128,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     PlanParams p, const int32_t* __restrict__ ctx_lens, const int32_t* __restrict__ cu,
     int32_t* __restrict__ hdr, SeqInfo* __restrict__ seqinfo, int32_t* __restrict__ split_base,
     int2* __restrict__ entries, int4* __restrict__ pre_jobs) {
-  __shared__ int s_err, s_tiles, s_max_full, s_split_keys;
+  __shared__ int s_err, s_tiles, s_max_full, s_split_keys, s_pre_first;
   __shared__ unsigned long long s_pre_keys, s_dec_keys;
   __shared__ int s_wave[3][kPlanThreads / 64];
   __shared__ int s_carry[3];
@@ -173,7 +173,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __syncthreads();
   if (s_err) {
     if (tid == 0) {
-      hdr[kHdrCounter] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
+      hdr[kHdrCounter] = 0; hdr[kHdrCounterPre] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
       hdr[kHdrError] = 1; hdr[kHdrNumItems] = 0; hdr[kHdrPreSplitKeys] = 0; hdr[kHdrNumPreJobs] = 0;
     }
     return;
@@ -191,6 +191,18 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       if (S >= s_max_full) S = 0;            // no tile would split
     }
     s_split_keys = (int)S;
+    // Mixed launches: how many workgroups take prefill items first (the others take decode items
+    // first).  Decode stays bound by HBM on fewer compute units, so prefill gets somewhat more
+    // than its share of the estimated work: 1.4 x share, in prefill and decode key-units weighted
+    // 3 : 2 as above.
+    int pre_first = 0;
+    if (p.mixed_grid > 0) {
+      const long long pu = 3LL * (long long)s_pre_keys * H;
+      const long long du = 2LL * (long long)s_dec_keys * H;
+      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (14LL * p.mixed_grid * pu) / (10 * (pu + du)))
+                              : p.mixed_grid;
+    }
+    s_pre_first = pre_first;
   }
   __syncthreads();
   const int S = s_split_keys;
@@ -269,6 +281,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const bool over = n_pre > p.max_pre || n_dec > p.max_dec || n_jobs > p.pre_jobs_cap ||
                       (n_jobs > 0 && (long long)n_pre * p.num_kv_heads > p.pre_slots);
     hdr[kHdrCounter] = 0;
+    hdr[kHdrCounterPre] = 0;
+    hdr[kHdrPreFirstWG] = s_pre_first;
     hdr[kHdrNumPre] = over ? 0 : n_pre;
     hdr[kHdrNumDec] = over ? 0 : n_dec;
     hdr[kHdrError] = over ? 2 : 0;
@@ -820,12 +834,36 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   const int n_pre = a.ws_hdr[kHdrNumPre];
   const int split_keys = a.ws_hdr[kHdrPreSplitKeys];
   const int H_kv = a.num_kv_heads;
-  if (threadIdx.x == 0) s_item[0] = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+  // Items: prefill items [0, n_pre * H_kv), decode items after them.  Prefill-only and
+  // decode-only launches hand them out with one counter.  Mixed launches keep a counter per kind;
+  // workgroups below kHdrPreFirstWG take prefill items first, the others decode items first, and
+  // each takes the other kind once its own is exhausted, so both kinds run side by side.
+  const int n_pre_items = n_pre * H_kv;
+  const bool pre_first = (int)blockIdx.x < a.ws_hdr[kHdrPreFirstWG];
+  auto claim = [&]() -> int {
+    if constexpr (kKinds != 3) {
+      return atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+    } else {
+      const int n_dec_items = n_items - n_pre_items;
+      if (pre_first) {
+        const int c = atomicAdd(&a.ws_hdr[kHdrCounterPre], 1);
+        if (c < n_pre_items) return c;
+        const int d = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+        return d < n_dec_items ? n_pre_items + d : n_items;
+      } else {
+        const int d = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+        if (d < n_dec_items) return n_pre_items + d;
+        const int c = atomicAdd(&a.ws_hdr[kHdrCounterPre], 1);
+        return c < n_pre_items ? c : n_items;
+      }
+    }
+  };
+  if (threadIdx.x == 0) s_item[0] = claim();
   __syncthreads();
   int slot = 0;
   int item = s_item[0];
   while (item < n_items) {
-    if (threadIdx.x == 0) s_item[slot ^ 1] = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
+    if (threadIdx.x == 0) s_item[slot ^ 1] = claim();
     const int e = item / H_kv;
     const int g = item - e * H_kv;
     if (e < n_pre) {
@@ -1007,6 +1045,11 @@ const DevCache& dev_cache() {
 }  // namespace
 
 int device_num_cu() { return dev_cache().num_cu; }
+
+int attention_grid(int head_dim, int kinds) {
+  const DevCache& c = dev_cache();
+  return c.num_cu * c.occ[head_dim == 128 ? 1 : 0][kinds];
+}
 
 hipError_t launch_plan(const PlanParams& p, const int32_t* ctx_lens, const int32_t* cu_q_lens,
                        void* workspace, const WsLayout& lay, hipStream_t stream) {

@@ -47,6 +47,8 @@ enum Hdr : int {
   kHdrNumItems = 4,    // (pre + dec) * H_kv
   kHdrPreSplitKeys = 5,  // keys per prefill split (a multiple of 64); 0 = tiles are not split
   kHdrNumPreJobs = 6,  // prefill tiles with more than one split (merge jobs)
+  kHdrCounterPre = 7,  // prefill work counter of mixed launches (atomic)
+  kHdrPreFirstWG = 8,  // mixed launches: workgroups [0, this) take prefill items first
   kHdrZero = 32,       // words 32..63: a zeroed 128-byte block (source for keys past the end)
   kHdrWords = 64
 };
@@ -82,6 +84,7 @@ struct PlanParams {
   int64_t max_dec;       // capacity of the decode entry list (and of the partial buffers)
   int64_t pre_slots;     // partial slots for split prefill items
   int64_t pre_jobs_cap;  // capacity of the prefill merge-job list
+  int mixed_grid;        // mixed launches: workgroups of the attention grid (0 otherwise)
 };
 
 struct AttnArgs {
@@ -115,6 +118,9 @@ WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_head
                           bool has_prefill);
 int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu);
 int device_num_cu();
+// Workgroups of a full persistent attention grid on the current device (compute units x
+// occupancy of the kernel for this head_dim and kinds).
+int attention_grid(int head_dim, int kinds);
 
 hipError_t launch_kv_append(const uint16_t* k_new, const uint16_t* v_new, uint16_t* k_pool,
                             uint16_t* v_pool, const int32_t* block_table, int bt_stride,
