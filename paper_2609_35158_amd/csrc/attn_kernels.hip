@@ -90,6 +90,13 @@ __device__ __forceinline__ int clamp_page(int p, int num_pages) {
   return p < 0 ? 0 : (p >= num_pages ? num_pages - 1 : p);
 }
 
+// The online softmax lets the running maximum m of a row lag the true maximum by up to kMaxLag
+// (log2 units): weights 2^(s c - m) then stay below 2^kMaxLag, which bf16 and the fp32 sums hold
+// as precisely as weights below 1.  A lane's 32 weights of a prefill stage summing to at most
+// kMaxWeightSum guarantees that bound without finding the stage's maximum.
+constexpr float kMaxLag = 8.0f;
+constexpr float kMaxWeightSum = 256.0f;             // 2^kMaxLag
+
 // LDS row strides (bytes) of staged K and V tiles: row = one key, padded against bank conflicts.
 // NW = waves per workgroup; kinds as in attn_kernel.
 template <int D, int NW, int kKinds> struct Lds {
@@ -449,37 +456,55 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
             if (key > row_limit) s[st][r] = -INFINITY;
           }
       }
-      // online softmax (base 2)
-      float mx = s[0][0];
-#pragma unroll
-      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
-#pragma unroll
-      for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-      mx = xor32_max(mx);
-      // the row maximum only moves when this tile exceeds it; the O rescale is skipped when no
-      // row of the wave moved (the largest weight of a row is then exactly 1 in bf16)
-      const bool grow = mx * c > m_run;
-      const float m_new = grow ? mx * c : m_run;
-      const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
-      float psum = 0.f;
+      // online softmax (base 2).  The weights are first taken against the running maximum m
+      // without looking for this stage's maximum; that is exact (any m gives the same softmax)
+      // as long as no weight exceeds 2^kMaxLag, which the lane's sum of its 32 weights bounds.
+      // Otherwise (the first stage of an item, where m is still -inf, or scores jumping more than
+      // kMaxLag above m) the stage is redone with the row maximum, and m moves to it only when it
+      // exceeds m by more than kMaxLag, so the O rescale is rare too.  A NaN sum (a masked key
+      // against m = -inf) also takes the redo.
+      float ps0 = 0.f, ps1 = 0.f;
       bf16x8 pop[2][2];
 #pragma unroll
       for (int st = 0; st < 2; ++st)
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
-          const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
-          psum += pv;
+          const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_run));
+          if (r & 1) ps1 += pv; else ps0 += pv;
           pop[st][r >> 3][r & 7] = (__bf16)pv;
         }
-      l_run = l_run * alpha + psum;
-      if (__ballot(grow)) {
-        __asm__ volatile("" ::);                   // a real branch, not a speculated rescale
+      float psum = ps0 + ps1;
+      if (__ballot(!(psum <= kMaxWeightSum))) {
+        __asm__ volatile("" ::);                   // a real branch
+        float mx = s[0][0];
 #pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
+        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
 #pragma unroll
-          for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
+        mx = xor32_max(mx);
+        const bool grow = mx * c > m_run + kMaxLag;
+        const float m_new = grow ? mx * c : m_run;
+        const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
+        ps0 = ps1 = 0.f;
+#pragma unroll
+        for (int st = 0; st < 2; ++st)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
+            if (r & 1) ps1 += pv; else ps0 += pv;
+            pop[st][r >> 3][r & 7] = (__bf16)pv;
+          }
+        psum = ps0 + ps1;
+        l_run *= alpha;
+        if (__ballot(grow)) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
+        }
+        m_run = m_new;
       }
-      m_run = m_new;
+      l_run += psum;
       // O^T += V^T P^T
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
@@ -644,7 +669,9 @@ __device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<
   float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])), fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const bool grow = mx * c > m_run;   // as in prefill_tile
+  // the maximum only moves when this page pair exceeds it, and the O rescale is skipped when no
+  // lane of the wave moved (decode is bound by HBM, so it keeps the exact maximum)
+  const bool grow = mx * c > m_run;
   const float m_new = grow ? mx * c : m_run;
   const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
   bf16x8 pop;
