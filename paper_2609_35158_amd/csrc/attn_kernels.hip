@@ -102,7 +102,9 @@ constexpr float kMaxWeightSum = 256.0f;             // 2^kMaxLag
 template <int D, int NW, int kKinds> struct Lds {
   static constexpr int kStride = D * 2 + 16;
   static constexpr int vStride = D * 2 + 64;   // 320 B at d=128: conflict-free transpose reads
-  static constexpr int prefill_bytes = (kKinds & 1) ? 2 * kKeysPerStage * (kStride + vStride) : 0;
+  // prefill-only kernels stage by LDS-DMA into four separate arrays; the mixed kernel carves its
+  // padded prefill buffers from the same region as the decode V buffers
+  static constexpr int prefill_bytes = (kKinds == 3) ? 2 * kKeysPerStage * (kStride + vStride) : 0;
   static constexpr int decode_v_bytes = NW * 2 * (2 * kPage * D * 2);   // per-wave double buffer
   static constexpr int merge_bytes = NW * 8 * D * 4 + 2 * NW * 8 * 4;
   // decode-only kernels keep their V buffers in separate arrays; the mixed kernel carves them here
@@ -299,6 +301,44 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
 }
 
+// 16 bytes per lane from global memory straight into LDS: lane l writes lds_base + 16 l.
+__device__ __forceinline__ void lds_dma16(const void* g, char* lds_base) {
+  __builtin_amdgcn_global_load_lds(g, (LDS_AS void*)((LDS_AS char*)(lds_base)), 16, 0, 0);
+}
+
+// The same copy issued as inline assembly, which the compiler does not track: it then inserts
+// no waits of its own for it (it would wait for every copy in flight before any LDS read), and
+// the caller waits with explicit vmcnt counts.  The compiler's own vmcnt waits stay correct,
+// because copies it does not know about can only make them wait longer.  lds_base must be
+// uniform across the wave.
+__device__ __forceinline__ void lds_dma16_untracked(const void* g, const char* lds_base) {
+  const unsigned lds = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)((LDS_AS const char*)lds_base));
+  __asm__ volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+}
+
+// vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
+#define PEARL_VMCNT(n) (((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
+
+// A prefill stage staged by LDS-DMA: kKeysPerStage key rows of D bf16, unpadded.  The 16-byte
+// chunk q of row r sits in slot q ^ swz(r), which keeps both operand read patterns free of bank
+// conflicts: the row reads of the Q.K products (16 consecutive rows, one chunk) and the
+// transposing reads of the P.V products (4 consecutive rows x 2 adjacent chunks).  Wave w copies
+// rows [RPW w, RPW w + RPW) of the stage, RPI rows per 64-lane DMA instruction.
+template <int D> struct DmaTile {
+  static_assert(D == 64 || D == 128, "head_dim");
+  static constexpr int CPR = D / 8;                 // 16-byte chunks per row
+  static constexpr int RB = D * 2;                  // bytes per row
+  static constexpr int BYTES = kKeysPerStage * RB;
+  static constexpr int RPI = 64 / CPR;              // rows per DMA instruction
+  static constexpr int RPW = kKeysPerStage / kWaves;   // rows copied per wave
+  static constexpr int NDMA = RPW / RPI;            // DMA instructions per wave and tensor
+  static_assert(NDMA >= 1 && NDMA * RPI == RPW && kPage % RPW == 0, "DMA split");
+  __device__ static __forceinline__ int swz(int r) {
+    if constexpr (D == 128) return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
+    else return (((r >> 1) & 1) << 1) | ((r >> 2) & 1) | (((r >> 3) & 1) << 2);
+  }
+};
+
 // ------------------------------------------------------------------------------------------------
 // Prefill-append work item: one (sequence, kv-head g, q-tile).  The tile holds 256 q-rows =
 // tokens_per_tile tokens x G heads of the group (row rho -> token rho / G, head rho % G), so every
@@ -312,17 +352,23 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
 // ------------------------------------------------------------------------------------------------
 // kHoistV: read the first dim block's V^T operands before the softmax (needs 16 more VGPRs; used
 // where the kernel has them to spare).
-template <int D, bool kHoistV>
+// kDma: stages travel by LDS-DMA into three DmaTile buffers per tensor, two stages ahead (no
+// staging registers, no LDS stores), which needs the buffers to be separate LDS objects;
+// otherwise they travel through registers into two padded buffers (rows KS, VS) carved from one
+// region (kb2 and vb2 unused).
+template <int D, bool kHoistV, bool kDma>
 __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
-                                             char* smem) {
+                                             char* kb0, char* kb1, char* kb2, char* vb0, char* vb1, char* vb2) {
   constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
   constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
   constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
   constexpr int CPR = D / 8;                        // 16-byte chunks per K/V row
   constexpr int NCH = kKeysPerStage * CPR / kThreads;  // chunks per thread per tensor per stage
   static_assert(NCH >= 1 && kKeysPerStage * CPR == NCH * kThreads, "staging split");
-  char* kbuf0 = smem;
-  char* vbuf0 = smem + 2 * kKeysPerStage * KS;
+  using DT = DmaTile<D>;
+  constexpr int RB = DT::RB;
+  auto kbuf = [&](int buf) { return buf == 0 ? kb0 : (buf == 1 ? kb1 : kb2); };
+  auto vbuf = [&](int buf) { return buf == 0 ? vb0 : (buf == 1 ? vb1 : vb2); };
 
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
@@ -390,9 +436,49 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
       S.v[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(a.v_pool) + base + toff[i]);
     }
   };
+  // DMA staging: per-lane byte offsets of the K operand rows (Q.K), the V^T transposing reads
+  // (P.V; rows krow and krow + 8 of each 16-key half) and the slots this lane fills by DMA
+  const int gi = lane >> 4, jl = lane & 15;
+  const int krow = 4 * (gi >> 1) + (jl >> 2);
+  const int dcol = 16 * (gi & 1) + 4 * (jl & 3);
+  int koff[kDma ? KB : 1], voff[2][kDma ? MB : 1], goff[kDma ? DT::NDMA : 1];
+  if constexpr (kDma) {
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) koff[kb] = (lane & 31) * RB + (((2 * kb + half) ^ DT::swz(lane & 15)) << 4);
+#pragma unroll
+    for (int sec = 0; sec < 2; ++sec)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb) {
+        const int r = krow + 8 * sec;
+        voff[sec][mb] = r * RB + ((((32 * mb + dcol) >> 3) ^ DT::swz(r)) << 4) + (jl & 1) * 8;
+      }
+#pragma unroll
+    for (int i = 0; i < DT::NDMA; ++i) {
+      const int r = DT::RPW * w + DT::RPI * i + lane / DT::CPR;   // stage row of this lane's slot
+      goff[i] = (r % kPage) * RB + (((lane % DT::CPR) ^ DT::swz(r)) << 4);
+    }
+  }
+  // This wave's rows of stage `step` (one page) by LDS-DMA.  Stages past the last needed key
+  // re-read a valid page; V rows past it come from the workspace's zero block (K rows there are
+  // always masked).
+  const char* zero_src = reinterpret_cast<const char*>(a.ws_hdr + kHdrZero);
+  auto dma_stage = [&](int step, int buf) {
+    const int pidx = min((step * kKeysPerStage + DT::RPW * w) / kPage, last_pidx);
+    const int page = clamp_page(bt_c[pidx], a.num_pages);
+    const size_t base = (((size_t)page * H_kv + g) * head_stride) * 2;
+    const char* ksrc = reinterpret_cast<const char*>(a.k_pool) + base;
+    const char* vsrc = reinterpret_cast<const char*>(a.v_pool) + base;
+#pragma unroll
+    for (int i = 0; i < DT::NDMA; ++i) {
+      const int key = step * kKeysPerStage + DT::RPW * w + DT::RPI * i + lane / DT::CPR;
+      const int row0 = DT::RPW * w + DT::RPI * i;
+      lds_dma16_untracked(ksrc + goff[i], kbuf(buf) + row0 * RB);
+      lds_dma16_untracked(key < kv_needed ? vsrc + goff[i] : zero_src, vbuf(buf) + row0 * RB);
+    }
+  };
   auto store_stage = [&](int step, int buf, const Stage& S) {
-    char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
-    char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
+    char* kb_ = kbuf(buf);
+    char* vb_ = vbuf(buf);
     if ((step + 1) * kKeysPerStage <= kv_needed) {   // every row of the stage is a needed key
 #pragma unroll
       for (int i = 0; i < NCH; ++i) {
@@ -414,8 +500,18 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
     }
   };
   auto compute = [&](int step, int buf) {
-      const char* kb_ = kbuf0 + buf * kKeysPerStage * KS;
-      const char* vb_ = vbuf0 + buf * kKeysPerStage * VS;
+      const char* kb_ = kbuf(buf);
+      const char* vb_ = vbuf(buf);
+      // byte offsets of a K operand row (sub-tile st, k block kb) and of a V^T transposing read
+      // (sub-tile st, 16-key half kk, dim block mb, row half sec)
+      auto koffset = [&](int st, int kb) {
+        if constexpr (kDma) return 32 * st * RB + koff[kb];
+        else return (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2;
+      };
+      auto voffset = [&](int st, int kk, int mb, int sec) {
+        if constexpr (kDma) return (32 * st + 16 * kk) * RB + voff[sec][mb];
+        else return (32 * st + 16 * kk + krow + 8 * sec) * VS + (32 * mb + dcol) * 2;
+      };
       const int k0 = step * kKeysPerStage;
 
       // S^T = K Q^T for two 32-key sub-tiles
@@ -425,23 +521,19 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
       for (int st = 0; st < 2; ++st) {
 #pragma unroll
         for (int kb = 0; kb < KB; ++kb) {
-          const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2);
+          const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + koffset(st, kb));
           s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
         }
       }
       // with kHoistV the V^T operands of the first 32-dim block are read now, so their LDS
       // latency hides behind the softmax instead of stalling the first P.V products
-      const int gi = lane >> 4, jl = lane & 15;
-      const int krow = 4 * (gi >> 1) + (jl >> 2);
-      const int dcol = 16 * (gi & 1) + 4 * (jl & 3);
       bf16x8 vfirst[2][2];
       if constexpr (kHoistV) {
 #pragma unroll
         for (int st = 0; st < 2; ++st)
 #pragma unroll
           for (int kk = 0; kk < 2; ++kk) {
-            const int off = (32 * st + 16 * kk + krow) * VS + dcol * 2;
-            vfirst[st][kk] = concat_tr(lds_read_tr(vb_, off), lds_read_tr(vb_, off + 8 * VS));
+            vfirst[st][kk] = concat_tr(lds_read_tr(vb_, voffset(st, kk, 0, 0)), lds_read_tr(vb_, voffset(st, kk, 0, 1)));
           }
       }
       // causal mask (only on steps that reach past some row's last visible key); the empty asm
@@ -516,13 +608,42 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
             if (kHoistV && mb == 0) {
               vop = vfirst[st][kk];
             } else {
-              const int off = (32 * st + 16 * kk + krow) * VS + (32 * mb + dcol) * 2;
-              vop = concat_tr(lds_read_tr(vb_, off), lds_read_tr(vb_, off + 8 * VS));
+              vop = concat_tr(lds_read_tr(vb_, voffset(st, kk, mb, 0)), lds_read_tr(vb_, voffset(st, kk, mb, 1)));
             }
             oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[st][kk], oacc[mb], 0, 0, 0);
           }
   };
 
+  if constexpr (kDma) {
+    // stage s sits in buffer (s - step_begin) % 3; its copy is issued two stages ahead, and the
+    // barrier closing stage s waits for the copy of stage s+1 only (the one of stage s+2 stays
+    // in flight).  The barrier is issued without the release fence of __syncthreads, which would
+    // drain every copy; all LDS reads of the stage have been consumed by then.
+    constexpr int kCopies = 2 * DT::NDMA;           // DMA instructions per stage and wave
+    auto close_stage = [&](bool copy_in_flight) {
+      if (copy_in_flight) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(kCopies));
+      else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
+      __asm__ volatile("s_barrier" ::: "memory");
+    };
+    // the prologue waits for everything (both first copies and this item's Q loads), so the
+    // compiler knows no load of its own is outstanding inside the loop
+    dma_stage(step_begin, 0);
+    if (step_begin + 1 < step_end) dma_stage(step_begin + 1, 1);
+    close_stage(false);
+    for (int step = step_begin; step < step_end; step += 3) {
+      if (step + 2 < step_end) dma_stage(step + 2, 2);
+      compute(step, 0);
+      close_stage(step + 2 < step_end);
+      if (step + 1 >= step_end) break;
+      if (step + 3 < step_end) dma_stage(step + 3, 0);
+      compute(step + 1, 1);
+      close_stage(step + 3 < step_end);
+      if (step + 2 >= step_end) break;
+      if (step + 4 < step_end) dma_stage(step + 4, 1);
+      compute(step + 2, 2);
+      close_stage(step + 4 < step_end);
+    }
+  } else {
   Stage sA, sB;
   const int last_step = step_end - 1;
   load_stage(step_begin, sA);
@@ -541,6 +662,7 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
     compute(step + 1, 1);
     if (step + 2 < step_end) store_stage(step + 2, 0, sA);
     __syncthreads();
+  }
   }
 
   // epilogue: combine the two half-row sums; a split item stores its fp32 partial state
@@ -613,9 +735,6 @@ template <int D> struct VTile {
   }
 };
 
-__device__ __forceinline__ void lds_dma16(const void* g, char* lds_base) {
-  __builtin_amdgcn_global_load_lds(g, (LDS_AS void*)((LDS_AS char*)(lds_base)), 16, 0, 0);
-}
 
 template <int D>
 __device__ __forceinline__ void decode_issue(const AttnArgs& a, int phys_a, int phys_b, bool pb_ok, int pa,
@@ -703,8 +822,6 @@ __device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<
   }
 }
 
-// vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
-#define PEARL_VMCNT(n) (((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
 
 // Page ids of the pair a wave will issue next, read with scalar loads from the block table.
 struct PairPages {
@@ -856,6 +973,8 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   __shared__ __attribute__((aligned(16))) char vbufB_[(kKinds == 2) ? NW * VTile<D>::PAIR_BYTES : 16];
   char* vbufA = (kKinds == 2) ? vbufA_ : smem;
   char* vbufB = (kKinds == 2) ? vbufB_ : smem + NW * VTile<D>::PAIR_BYTES;
+  constexpr int kDT = (kKinds == 1) ? DmaTile<D>::BYTES : 16;
+  __shared__ __attribute__((aligned(16))) char pk0[kDT], pk1[kDT], pk2[kDT], pv0[kDT], pv1[kDT], pv2[kDT];
   __shared__ int s_item[2];
   const int n_items = a.ws_hdr[kHdrNumItems];
   const int n_pre = a.ws_hdr[kHdrNumPre];
@@ -897,7 +1016,14 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
       if constexpr ((kKinds & 1) != 0) {
         static_assert(NW == kWaves, "prefill tiles use 8 waves");
         const int2 en = a.entries[e];
-        prefill_tile<D, kKinds == 1>(a, e, en.x, en.y, g, split_keys, smem);
+        if constexpr (kKinds == 1) {
+          prefill_tile<D, true, true>(a, e, en.x, en.y, g, split_keys, pk0, pk1, pk2, pv0, pv1, pv2);
+        } else {
+          constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
+          char* vb = smem + 2 * kKeysPerStage * KS;
+          prefill_tile<D, false, false>(a, e, en.x, en.y, g, split_keys, smem, smem + kKeysPerStage * KS, nullptr,
+                                        vb, vb + kKeysPerStage * VS, nullptr);
+        }
       }
     } else {
       if constexpr ((kKinds & 2) != 0) {
