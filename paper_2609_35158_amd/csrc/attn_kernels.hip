@@ -97,14 +97,12 @@ __device__ __forceinline__ int clamp_page(int p, int num_pages) {
 constexpr float kMaxLag = 8.0f;
 constexpr float kMaxWeightSum = 256.0f;             // 2^kMaxLag
 
-// LDS row strides (bytes) of staged K and V tiles: row = one key, padded against bank conflicts.
-// NW = waves per workgroup; kinds as in attn_kernel.
+// LDS of the attention kernel beyond its separate arrays.  NW = waves per workgroup; kinds as
+// in attn_kernel.
 template <int D, int NW, int kKinds> struct Lds {
-  static constexpr int kStride = D * 2 + 16;
-  static constexpr int vStride = D * 2 + 64;   // 320 B at d=128: conflict-free transpose reads
-  // prefill-only kernels stage by LDS-DMA into four separate arrays; the mixed kernel carves its
-  // padded prefill buffers from the same region as the decode V buffers
-  static constexpr int prefill_bytes = (kKinds == 3) ? 2 * kKeysPerStage * (kStride + vStride) : 0;
+  // prefill stages travel by LDS-DMA into six stage buffers (three K, three V): separate arrays
+  // in prefill-only kernels, carved from the region of the decode V buffers in the mixed kernel
+  static constexpr int prefill_bytes = (kKinds == 3) ? 6 * kKeysPerStage * D * 2 : 0;
   static constexpr int decode_v_bytes = NW * 2 * (2 * kPage * D * 2);   // per-wave double buffer
   static constexpr int merge_bytes = NW * 8 * D * 4 + 2 * NW * 8 * 4;
   // decode-only kernels keep their V buffers in separate arrays; the mixed kernel carves them here
@@ -309,11 +307,21 @@ __device__ __forceinline__ void lds_dma16(const void* g, char* lds_base) {
 // The same copy issued as inline assembly, which the compiler does not track: it then inserts
 // no waits of its own for it (it would wait for every copy in flight before any LDS read), and
 // the caller waits with explicit vmcnt counts.  The compiler's own vmcnt waits stay correct,
-// because copies it does not know about can only make them wait longer.  lds_base must be
-// uniform across the wave.
+// because copies it does not know about can only make them wait longer.  The LDS base goes
+// through M0, which the sequence saves and restores (the copy reads it at issue, one wait state
+// after it is written).  lds_base must be uniform across the wave.
 __device__ __forceinline__ void lds_dma16_untracked(const void* g, const char* lds_base) {
   const unsigned lds = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)((LDS_AS const char*)lds_base));
-  __asm__ volatile("s_mov_b32 m0, %1\n\tglobal_load_lds_dwordx4 %0, off" ::"v"(g), "s"(lds) : "memory", "m0");
+  unsigned saved;
+  __asm__ volatile(
+      "s_mov_b32 %0, m0\n\t"
+      "s_mov_b32 m0, %2\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off\n\t"
+      "s_mov_b32 m0, %0"
+      : "=&s"(saved)
+      : "v"(g), "s"(lds)
+      : "memory");
 }
 
 // vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
@@ -352,19 +360,12 @@ template <int D> struct DmaTile {
 // ------------------------------------------------------------------------------------------------
 // kHoistV: read the first dim block's V^T operands before the softmax (needs 16 more VGPRs; used
 // where the kernel has them to spare).
-// kDma: stages travel by LDS-DMA into three DmaTile buffers per tensor, two stages ahead (no
-// staging registers, no LDS stores), which needs the buffers to be separate LDS objects;
-// otherwise they travel through registers into two padded buffers (rows KS, VS) carved from one
-// region (kb2 and vb2 unused).
-template <int D, bool kHoistV, bool kDma>
+// Stages travel by LDS-DMA into three DmaTile buffers per tensor (kb*, vb*), two stages ahead.
+template <int D, bool kHoistV>
 __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
                                              char* kb0, char* kb1, char* kb2, char* vb0, char* vb1, char* vb2) {
-  constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
   constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
   constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
-  constexpr int CPR = D / 8;                        // 16-byte chunks per K/V row
-  constexpr int NCH = kKeysPerStage * CPR / kThreads;  // chunks per thread per tensor per stage
-  static_assert(NCH >= 1 && kKeysPerStage * CPR == NCH * kThreads, "staging split");
   using DT = DmaTile<D>;
   constexpr int RB = DT::RB;
   auto kbuf = [&](int buf) { return buf == 0 ? kb0 : (buf == 1 ? kb1 : kb2); };
@@ -409,54 +410,27 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   const int step_begin = split * (split_keys / kKeysPerStage);
   const int step_end = split + 1 < n_split ? step_begin + split_keys / kKeysPerStage : n_steps;
 
-  // K/V staging: chunk i of this thread is 16 bytes of key row kk = cidx / CPR of the stage; the
-  // stage's page index of that row is the same for the whole wave, so it comes from a scalar
-  // load of the block table.  Loads are unconditional (rows past the last needed key re-read a
-  // valid page and are zeroed when stored to LDS) and run two stages ahead of the compute.
   const ConstI32Ptr bt_c = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
   const int last_pidx = (kv_needed - 1) / kPage;
-  struct Stage { u32x4 k[NCH], v[NCH]; };
-  // byte offset of this thread's chunk i inside its (page, kv-head) block: constant over stages
-  // (stages start on page boundaries); the block's base is uniform per wave, so each load is a
-  // scalar base plus one 32-bit vector offset
-  uint32_t toff[NCH];
-#pragma unroll
-  for (int i = 0; i < NCH; ++i) {
-    const int cidx = threadIdx.x + i * kThreads;
-    const int kk = cidx / CPR, dc = cidx - kk * CPR;
-    toff[i] = (uint32_t)(((kk % kPage) * D + dc * 8) * 2);
-  }
-  auto load_stage = [&](int step, Stage& S) {
-#pragma unroll
-    for (int i = 0; i < NCH; ++i) {
-      const int pidx = min(step * (kKeysPerStage / kPage) + (64 * w + kThreads * i) / (kPage * CPR), last_pidx);
-      const int page = clamp_page(bt_c[pidx], a.num_pages);
-      const size_t base = (((size_t)page * H_kv + g) * head_stride) * 2;
-      S.k[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(a.k_pool) + base + toff[i]);
-      S.v[i] = *reinterpret_cast<const u32x4*>(reinterpret_cast<const char*>(a.v_pool) + base + toff[i]);
-    }
-  };
-  // DMA staging: per-lane byte offsets of the K operand rows (Q.K), the V^T transposing reads
-  // (P.V; rows krow and krow + 8 of each 16-key half) and the slots this lane fills by DMA
+  // per-lane byte offsets of the K operand rows (Q.K), of the V^T transposing reads (P.V; rows
+  // krow and krow + 8 of each 16-key half) and of the slots this lane fills by DMA
   const int gi = lane >> 4, jl = lane & 15;
   const int krow = 4 * (gi >> 1) + (jl >> 2);
   const int dcol = 16 * (gi & 1) + 4 * (jl & 3);
-  int koff[kDma ? KB : 1], voff[2][kDma ? MB : 1], goff[kDma ? DT::NDMA : 1];
-  if constexpr (kDma) {
+  int koff[KB], voff[2][MB], goff[DT::NDMA];
 #pragma unroll
-    for (int kb = 0; kb < KB; ++kb) koff[kb] = (lane & 31) * RB + (((2 * kb + half) ^ DT::swz(lane & 15)) << 4);
+  for (int kb = 0; kb < KB; ++kb) koff[kb] = (lane & 31) * RB + (((2 * kb + half) ^ DT::swz(lane & 15)) << 4);
 #pragma unroll
-    for (int sec = 0; sec < 2; ++sec)
+  for (int sec = 0; sec < 2; ++sec)
 #pragma unroll
-      for (int mb = 0; mb < MB; ++mb) {
-        const int r = krow + 8 * sec;
-        voff[sec][mb] = r * RB + ((((32 * mb + dcol) >> 3) ^ DT::swz(r)) << 4) + (jl & 1) * 8;
-      }
-#pragma unroll
-    for (int i = 0; i < DT::NDMA; ++i) {
-      const int r = DT::RPW * w + DT::RPI * i + lane / DT::CPR;   // stage row of this lane's slot
-      goff[i] = (r % kPage) * RB + (((lane % DT::CPR) ^ DT::swz(r)) << 4);
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = krow + 8 * sec;
+      voff[sec][mb] = r * RB + ((((32 * mb + dcol) >> 3) ^ DT::swz(r)) << 4) + (jl & 1) * 8;
     }
+#pragma unroll
+  for (int i = 0; i < DT::NDMA; ++i) {
+    const int r = DT::RPW * w + DT::RPI * i + lane / DT::CPR;   // stage row of this lane's slot
+    goff[i] = (r % kPage) * RB + (((lane % DT::CPR) ^ DT::swz(r)) << 4);
   }
   // This wave's rows of stage `step` (one page) by LDS-DMA.  Stages past the last needed key
   // re-read a valid page; V rows past it come from the workspace's zero block (K rows there are
@@ -476,42 +450,13 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
       lds_dma16_untracked(key < kv_needed ? vsrc + goff[i] : zero_src, vbuf(buf) + row0 * RB);
     }
   };
-  auto store_stage = [&](int step, int buf, const Stage& S) {
-    char* kb_ = kbuf(buf);
-    char* vb_ = vbuf(buf);
-    if ((step + 1) * kKeysPerStage <= kv_needed) {   // every row of the stage is a needed key
-#pragma unroll
-      for (int i = 0; i < NCH; ++i) {
-        const int cidx = threadIdx.x + i * kThreads;
-        const int kk = cidx / CPR, dc = cidx - kk * CPR;
-        *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = S.k[i];
-        *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = S.v[i];
-      }
-    } else {
-      const u32x4 zero = u32x4{0u, 0u, 0u, 0u};
-#pragma unroll
-      for (int i = 0; i < NCH; ++i) {
-        const int cidx = threadIdx.x + i * kThreads;
-        const int kk = cidx / CPR, dc = cidx - kk * CPR;
-        const bool ok = step * kKeysPerStage + kk < kv_needed;
-        *reinterpret_cast<u32x4*>(kb_ + kk * KS + dc * 16) = ok ? S.k[i] : zero;
-        *reinterpret_cast<u32x4*>(vb_ + kk * VS + dc * 16) = ok ? S.v[i] : zero;
-      }
-    }
-  };
   auto compute = [&](int step, int buf) {
       const char* kb_ = kbuf(buf);
       const char* vb_ = vbuf(buf);
       // byte offsets of a K operand row (sub-tile st, k block kb) and of a V^T transposing read
       // (sub-tile st, 16-key half kk, dim block mb, row half sec)
-      auto koffset = [&](int st, int kb) {
-        if constexpr (kDma) return 32 * st * RB + koff[kb];
-        else return (32 * st + (lane & 31)) * KS + (16 * kb + 8 * half) * 2;
-      };
-      auto voffset = [&](int st, int kk, int mb, int sec) {
-        if constexpr (kDma) return (32 * st + 16 * kk) * RB + voff[sec][mb];
-        else return (32 * st + 16 * kk + krow + 8 * sec) * VS + (32 * mb + dcol) * 2;
-      };
+      auto koffset = [&](int st, int kb) { return 32 * st * RB + koff[kb]; };
+      auto voffset = [&](int st, int kk, int mb, int sec) { return (32 * st + 16 * kk) * RB + voff[sec][mb]; };
       const int k0 = step * kKeysPerStage;
 
       // S^T = K Q^T for two 32-key sub-tiles
@@ -614,55 +559,33 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
           }
   };
 
-  if constexpr (kDma) {
-    // stage s sits in buffer (s - step_begin) % 3; its copy is issued two stages ahead, and the
-    // barrier closing stage s waits for the copy of stage s+1 only (the one of stage s+2 stays
-    // in flight).  The barrier is issued without the release fence of __syncthreads, which would
-    // drain every copy; all LDS reads of the stage have been consumed by then.
-    constexpr int kCopies = 2 * DT::NDMA;           // DMA instructions per stage and wave
-    auto close_stage = [&](bool copy_in_flight) {
-      if (copy_in_flight) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(kCopies));
-      else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
-      __asm__ volatile("s_barrier" ::: "memory");
-    };
-    // the prologue waits for everything (both first copies and this item's Q loads), so the
-    // compiler knows no load of its own is outstanding inside the loop
-    dma_stage(step_begin, 0);
-    if (step_begin + 1 < step_end) dma_stage(step_begin + 1, 1);
-    close_stage(false);
-    for (int step = step_begin; step < step_end; step += 3) {
-      if (step + 2 < step_end) dma_stage(step + 2, 2);
-      compute(step, 0);
-      close_stage(step + 2 < step_end);
-      if (step + 1 >= step_end) break;
-      if (step + 3 < step_end) dma_stage(step + 3, 0);
-      compute(step + 1, 1);
-      close_stage(step + 3 < step_end);
-      if (step + 2 >= step_end) break;
-      if (step + 4 < step_end) dma_stage(step + 4, 1);
-      compute(step + 2, 2);
-      close_stage(step + 4 < step_end);
-    }
-  } else {
-  Stage sA, sB;
-  const int last_step = step_end - 1;
-  load_stage(step_begin, sA);
-  load_stage(min(step_begin + 1, last_step), sB);
-  store_stage(step_begin, 0, sA);
-  __syncthreads();
-  for (int step = step_begin; step < step_end; step += 2) {
-    // even step: sB holds step+1 (in flight); refill sA with step+2 (past the end: a repeat)
-    load_stage(min(step + 2, last_step), sA);
+  // stage s sits in buffer (s - step_begin) % 3; its copy is issued two stages ahead, and the
+  // barrier closing stage s waits for the copy of stage s+1 only (the one of stage s+2 stays
+  // in flight).  The barrier is issued without the release fence of __syncthreads, which would
+  // drain every copy; all LDS reads of the stage have been consumed by then.
+  constexpr int kCopies = 2 * DT::NDMA;           // DMA instructions per stage and wave
+  auto close_stage = [&](bool copy_in_flight) {
+    if (copy_in_flight) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(kCopies));
+    else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
+    __asm__ volatile("s_barrier" ::: "memory");
+  };
+  // the prologue waits for everything (both first copies and this item's Q loads), so the
+  // compiler knows no load of its own is outstanding inside the loop
+  dma_stage(step_begin, 0);
+  if (step_begin + 1 < step_end) dma_stage(step_begin + 1, 1);
+  close_stage(false);
+  for (int step = step_begin; step < step_end; step += 3) {
+    if (step + 2 < step_end) dma_stage(step + 2, 2);
     compute(step, 0);
-    if (step + 1 < step_end) store_stage(step + 1, 1, sB);
-    __syncthreads();
+    close_stage(step + 2 < step_end);
     if (step + 1 >= step_end) break;
-    // odd step: sA holds step+2; refill sB with step+3
-    load_stage(min(step + 3, last_step), sB);
+    if (step + 3 < step_end) dma_stage(step + 3, 0);
     compute(step + 1, 1);
-    if (step + 2 < step_end) store_stage(step + 2, 0, sA);
-    __syncthreads();
-  }
+    close_stage(step + 3 < step_end);
+    if (step + 2 >= step_end) break;
+    if (step + 4 < step_end) dma_stage(step + 4, 1);
+    compute(step + 2, 2);
+    close_stage(step + 4 < step_end);
   }
 
   // epilogue: combine the two half-row sums; a split item stores its fp32 partial state
@@ -1017,14 +940,15 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
         static_assert(NW == kWaves, "prefill tiles use 8 waves");
         const int2 en = a.entries[e];
         if constexpr (kKinds == 1) {
-          prefill_tile<D, true, true>(a, e, en.x, en.y, g, split_keys, pk0, pk1, pk2, pv0, pv1, pv2);
+          prefill_tile<D, true>(a, e, en.x, en.y, g, split_keys, pk0, pk1, pk2, pv0, pv1, pv2);
         } else {
-          constexpr int KS = Lds<D, kWaves, 1>::kStride, VS = Lds<D, kWaves, 1>::vStride;
-          char* vb = smem + 2 * kKeysPerStage * KS;
-          prefill_tile<D, false, false>(a, e, en.x, en.y, g, split_keys, smem, smem + kKeysPerStage * KS, nullptr,
-                                        vb, vb + kKeysPerStage * VS, nullptr);
-        }
-      }
+          // the mixed kernel's stage buffers share its LDS region with the decode V buffers (a
+          // workgroup runs one item at a time, and items are separated by a drained barrier)
+          constexpr int B = DmaTile<D>::BYTES;
+          static_assert(6 * B <= Lds<D, NW, kKinds>::bytes, "stage buffers fit the shared region");
+          prefill_tile<D, false>(a, e, en.x, en.y, g, split_keys, smem, smem + B, smem + 2 * B,
+                                       smem + 3 * B, smem + 4 * B, smem + 5 * B);
+        }      }
     } else {
       if constexpr ((kKinds & 2) != 0) {
         const int2 en = a.entries[max_pre + (e - n_pre)];
