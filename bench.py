@@ -9,12 +9,22 @@ merge).  value = decode tokens/s for the layer = 64 / step time.
 
 The same line carries:
   roofline      HBM roofline of the dominant kernel (the attention kernel), timed with HIP
-                events around each launch inside the timed region;
-  cpu_baseline  the CPU oracle (numpy float64) timed on this host on a bounded sample;
+                events around each launch inside the timed region (mean, median, min), against
+                the published peak and against the bandwidth the library's streaming kernels
+                reach in the same run (hbm_measured);
+  counters      clock, MFMA use and occupancy of the decode and prefill kernels from the
+                committed rocprofv3 counter pass (while the kernel source is unchanged);
+  cpu_baseline  the CPU oracle (numpy float64) timed on this host by a pool of single-threaded
+                worker processes, one per core, on a bounded sample;
   secondary     prefill-append TFLOP/s (Qwen3-8B shape), Qwen3-30B-A3B-shaped decode at batch
                 256/128/32, the colocated mixed batch, kv_append GB/s, KV transfer pack/unpack
                 GB/s, a decode/prefill interference sweep (one mixed launch vs decode alone
                 as prefill chunks grow), and the PD decision engine calibrated from the kernels.
+
+Timing: consecutive timed steps use different copies of their inputs, so no step finds its K/V
+in L2 or the 256 MiB Infinity Cache; launches timed on sub-batches (interference sweep, engine
+calibration, KV transfer) are each preceded by a cache flush (a 1 GiB read) outside their
+events.
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--no-secondary] [--no-cpu]
 """
@@ -101,25 +111,39 @@ class EventPairs:
         a, b = self.ev[i]
         return a.cuda_event, b.cuda_event
 
-    def mean_ms(self, n):
-        return sum(a.elapsed_time(b) for a, b in self.ev[:n]) / n
+    def times_ms(self, n):
+        return [a.elapsed_time(b) for a, b in self.ev[:n]]
 
 
-def run_timed(torch, pa, step, steps, warmup):
+def run_timed(torch, pa, step, steps, warmup, flush=None):
     """Run `warmup` untimed steps, then `steps` timed steps bracketed by synchronize.  `step(hook)`
-    performs one step and calls hook() right before the library call whose kernel is timed."""
+    performs one step and calls hook() right before the library call whose kernel is timed.
+    With `flush` (a callable enqueuing the cache flush) every step is preceded by a flush, which
+    the kernel events do not include (the wall-clock step time then does).
+    Returns (wall ms per step, mean kernel ms, per-launch kernel ms)."""
     pairs = EventPairs(torch, steps)
     for _ in range(warmup):
+        if flush:
+            flush()
         step(lambda: None)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(steps):
+        if flush:
+            flush()
         h = pairs.handles(i)
         step(lambda h=h: pa.binding.set_kernel_events(*h))
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     pa.binding.set_kernel_events(None, None)
-    return (t1 - t0) * 1e3 / steps, pairs.mean_ms(steps)
+    times = pairs.times_ms(steps)
+    return (t1 - t0) * 1e3 / steps, sum(times) / len(times), times
+
+
+def launch_stats(times):
+    """Median and minimum of per-launch kernel times (ms)."""
+    import numpy as np
+    return {"kernel_ms_median": round(float(np.median(times)), 5), "kernel_ms_min": round(float(min(times)), 5)}
 
 
 # ------------------------------------------------------------------------------------------------
@@ -173,6 +197,42 @@ def make_step(torch, pa, case, mode):
     return step, out
 
 
+# Consecutive timed steps read different copies of the inputs: between two uses of one copy the
+# steps read at least this many bytes of the others, more than L2 (4 MiB per XCD) and the 256 MiB
+# Infinity Cache hold, so no step finds its K/V cached by the previous one.
+REPLICA_MIN_OTHER_BYTES = 1 << 30
+
+
+def input_bytes(case):
+    return sum(t.numel() * t.element_size() for t in (case.k_pool, case.v_pool, case.q, case.k_new, case.v_new))
+
+
+def make_replicas(torch, case):
+    """The case plus copies of its device inputs (pools, q, new K/V; lengths and block table are
+    shared), enough of them that the others total at least REPLICA_MIN_OTHER_BYTES."""
+    import dataclasses
+    n = max(2, 1 + -(-REPLICA_MIN_OTHER_BYTES // input_bytes(case)))
+    reps = [case]
+    for _ in range(n - 1):
+        reps.append(dataclasses.replace(case, k_pool=case.k_pool.clone(), v_pool=case.v_pool.clone(),
+                                        q=case.q.clone(), k_new=case.k_new.clone(), v_new=case.v_new.clone()))
+    return reps
+
+
+def make_rotating_step(torch, pa, case, mode):
+    """make_step over the replicas of `case`, used in turn.  Every replica holds the same bytes, so
+    every step computes the same result; returns (step, out of the first replica, replicas)."""
+    reps = make_replicas(torch, case)
+    made = [make_step(torch, pa, c, mode) for c in reps]
+    state = {"i": 0}
+
+    def step(hook, attention=True, append=True):
+        st = made[state["i"] % len(made)][0]
+        state["i"] += 1
+        st(hook, attention=attention, append=append)
+    return step, made[0][1], reps
+
+
 def time_append(torch, pa, step, steps):
     def one(hook):
         hook()
@@ -181,37 +241,88 @@ def time_append(torch, pa, step, steps):
     return run_timed(torch, pa, one, steps, 1)
 
 
-def time_graph_step(torch, pa, case, steps, warmup):
-    """The same decode step (kv_append + decode) captured once in a HIP graph and replayed: the
-    library synchronises nothing and allocates nothing, so the whole step is capturable."""
+def time_graph_step(torch, pa, cases, steps, warmup):
+    """The same decode step (kv_append + decode) captured in a HIP graph, once per replica, and
+    replayed: the library synchronises nothing and allocates nothing, so the whole step is
+    capturable.  Returns ms per step."""
     import numpy as np
+    from paper_2609_35158_amd import binding as bd
+    case = cases[0]
     ctx = torch.from_numpy(case.ctx_lens.astype(np.int32)).cuda()
     max_kv = int(case.kv_lens.max())
-    out = torch.empty_like(case.q)
-    from paper_2609_35158_amd import binding as bd
+    outs = [torch.empty_like(c.q) for c in cases]
     desc = bd.make_desc(case.block_table, ctx, None, case.batch, 1, max_kv)
     ws = torch.empty(bd.workspace_bytes(case.num_q_heads, case.k_pool, desc), dtype=torch.uint8, device="cuda")
 
     def step():
-        pa.kv_append(case.k_new, case.v_new, case.k_pool, case.v_pool, case.block_table, ctx, None, 1, max_kv)
-        pa.decode(case.q, case.k_pool, case.v_pool, case.block_table, ctx, max_kv, scale=case.scale,
-                  out=out, workspace=ws)
+        for c, out in zip(cases, outs):
+            pa.kv_append(c.k_new, c.v_new, c.k_pool, c.v_pool, c.block_table, ctx, None, 1, max_kv)
+            pa.decode(c.q, c.k_pool, c.v_pool, c.block_table, ctx, max_kv, scale=c.scale, out=out, workspace=ws)
 
     step()
     torch.cuda.synchronize()
     graph = torch.cuda.CUDAGraph()
     with torch.cuda.graph(graph):
         step()
-    for _ in range(warmup):
+    replays = max(1, -(-steps // len(cases)))
+    for _ in range(max(1, -(-warmup // len(cases)))):
         graph.replay()
     torch.cuda.synchronize()
     t0 = time.perf_counter()
-    for _ in range(steps):
+    for _ in range(replays):
         graph.replay()
     torch.cuda.synchronize()
-    ms = (time.perf_counter() - t0) * 1e3 / steps
-    del graph, out, ws
+    ms = (time.perf_counter() - t0) * 1e3 / (replays * len(cases))
+    del graph, outs, ws
     return ms
+
+
+# ------------------------------------------------------------------------------------------------
+# achievable HBM bandwidth and the cache flush
+# ------------------------------------------------------------------------------------------------
+
+def hbm_probe(torch, nbytes=1 << 30, reps=10):
+    """Bandwidth this device reaches with the library's streaming kernels over `nbytes` buffers:
+    read-only, write-only and copy (bytes read + written), median of `reps` launches, each
+    launched after a flush.  Returns (figures, flush callable, buffers to keep)."""
+    import numpy as np
+    from paper_2609_35158_amd import binding as bd
+    src = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    dst = torch.empty_like(src)
+    scratch = torch.empty_like(src)
+    sink = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    bd.hbm_fill(src, 0x3F803F80)
+    bd.hbm_fill(scratch, 0)
+
+    def flush():
+        # a read, not a write: a written flush leaves dirty lines whose write-back would land in
+        # the next timed kernel (measured: a read after a 1 GiB written flush runs 25% slower)
+        bd.hbm_read(scratch, sink)
+
+    def timed(fn):
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for _ in range(2):
+            flush()
+            fn()
+        for a, b in ev:
+            flush()
+            a.record()
+            fn()
+            b.record()
+        torch.cuda.synchronize()
+        t = [a.elapsed_time(b) for a, b in ev]
+        return float(np.median(t)), float(min(t))
+    t_read = timed(lambda: bd.hbm_read(src, sink))
+    t_write = timed(lambda: bd.hbm_fill(dst, 0x11111111))
+    t_copy = timed(lambda: bd.hbm_copy(src, dst))
+    gbps = lambda moved, t: round(moved / (t * 1e-3) / 1e9, 1)
+    fig = {"bytes": nbytes, "what": "library streaming kernels (pearl_hbm_read / _fill / _copy), 16-byte "
+                                    "vectors, median of %d launches each after a 1 GiB read flush" % reps,
+           "read_GBps": gbps(nbytes, t_read[0]), "write_GBps": gbps(nbytes, t_write[0]),
+           "copy_GBps": gbps(2 * nbytes, t_copy[0]),
+           "read_GBps_best": gbps(nbytes, t_read[1]), "copy_GBps_best": gbps(2 * nbytes, t_copy[1])}
+    del src, dst
+    return fig, flush, (scratch, sink)
 
 
 # ------------------------------------------------------------------------------------------------
@@ -222,7 +333,7 @@ PD_CHUNKS = (1, 2, 4, 8, 16)
 PD_SIZES = (256, 512, 1024, 2048)
 
 
-def pd_interference(torch, pa, workloads, steps, warmup):
+def pd_interference(torch, pa, workloads, steps, warmup, flush=None):
     """Cost of colocating prefill with decode inside one launch (the kernel-level analogue of the
     paper's observation that prefill insertions stall the decode batch; Motivation, PD
     interference figure).  A fixed Qwen3-30B-A3B-shaped decode batch -- 192 sequences, contexts
@@ -239,7 +350,7 @@ def pd_interference(torch, pa, workloads, steps, warmup):
 
     def time_attn(case, mode):
         st, out = make_step(torch, pa, case, mode)
-        _, ms_k = run_timed(torch, pa, lambda hook: st(hook, append=False), steps, warmup)
+        _, ms_k, _ = run_timed(torch, pa, lambda hook: st(hook, append=False), steps, warmup, flush)
         del st, out
         return ms_k
 
@@ -293,7 +404,7 @@ def pd_interference(torch, pa, workloads, steps, warmup):
 # KV transfer between pools (pack on the sending pool, unpack into the receiving pool)
 # ------------------------------------------------------------------------------------------------
 
-def kv_transfer(torch, pa, workloads, steps, warmup):
+def kv_transfer(torch, pa, workloads, steps, warmup, flush=None):
     """Pack/unpack GB/s (algorithmic bytes = rows read + rows written) for two transfers on the
     Qwen3-8B shape: whole contexts of the 64-sequence decode batch (2.4 GB of K/V, e.g. moving
     trajectories between decode workers), and one turn's new tokens of the 16-sequence
@@ -323,8 +434,8 @@ def kv_transfer(torch, pa, workloads, steps, warmup):
         pack = lambda hook: (hook(), pa.kv_pack(case.k_pool, case.v_pool, case.block_table, st_d, cu_d,
                                                 total, max_q, max_kv, out=buf))
         unpack = lambda hook: (hook(), pa.kv_unpack(buf, kp_b, vp_b, bt_b, st_d, cu_d, max_q, max_kv))
-        _, ms_pack = run_timed(torch, pa, pack, steps, warmup)
-        _, ms_unpack = run_timed(torch, pa, unpack, steps, warmup)
+        _, ms_pack, _ = run_timed(torch, pa, pack, steps, warmup, flush)
+        _, ms_unpack, _ = run_timed(torch, pa, unpack, steps, warmup, flush)
         moved = 2 * buf.numel() * 2            # read + write, bytes
         e = {"workload": name, "mode": "kv-transfer", "tokens": total, "buffer_bytes": buf.numel() * 2,
              "pack_ms": round(ms_pack, 5), "unpack_ms": round(ms_unpack, 5),
@@ -360,7 +471,7 @@ PD_INPUTS = {"B": 64.0, "S": 40.0, "dL": 600.0, "r": 300.0, "T_env": 120.0,
 PD_PROFILES = {"bubbly": {"theta": 0.3, "T_over": 0.05}, "interfering": {"theta": 0.05, "T_over": 1.0}}
 
 
-def pd_engine(torch, pa, workloads, steps, warmup):
+def pd_engine(torch, pa, workloads, steps, warmup, flush=None):
     """Calibrate the makespan-model costs from this GPU's kernels (decode attention time vs batch
     -> A_attn, b_attn per layer; prefill attention time vs new tokens -> per-token time), refit
     with the library's own telemetry refits, scale to whole models, then run the decision engine
@@ -370,7 +481,7 @@ def pd_engine(torch, pa, workloads, steps, warmup):
 
     def attn_ms(case, mode):
         st, out = make_step(torch, pa, case, mode)
-        _, ms = run_timed(torch, pa, lambda hook: st(hook, append=False), steps, warmup)
+        _, ms, _ = run_timed(torch, pa, lambda hook: st(hook, append=False), steps, warmup, flush)
         del st, out
         return ms
 
@@ -473,62 +584,163 @@ def pd_engine(torch, pa, workloads, steps, warmup):
 # CPU oracle baseline on a bounded sample
 # ------------------------------------------------------------------------------------------------
 
-def compact_pool(torch, case, seqs):
-    import numpy as np
-    bt = case.block_table.cpu().numpy()
-    npages = (case.kv_lens + 15) // 16
-    uniq = np.unique(np.concatenate([bt[b, :npages[b]] for b in seqs]))
-    remap = {int(p): i for i, p in enumerate(uniq)}
-    idx = torch.from_numpy(uniq.astype(np.int64)).cuda()
-    as_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-    kp = as_bits(case.k_pool.index_select(0, idx))
-    vp = as_bits(case.v_pool.index_select(0, idx))
-    sub_bt = np.zeros((len(seqs), int(npages[list(seqs)].max())), np.int32)
-    for i, b in enumerate(seqs):
-        sub_bt[i, :npages[b]] = [remap[int(p)] for p in bt[b, :npages[b]]]
-    return kp, vp, sub_bt
+BLAS_THREAD_VARS = ("OMP_NUM_THREADS", "OPENBLAS_NUM_THREADS", "MKL_NUM_THREADS", "BLIS_NUM_THREADS")
 
 
-def cpu_baseline(torch, case, out, budget_s):
-    """Time the oracle (single BLAS thread) decoding whole sequences of the same workload, in a
-    random order, passing over the batch again until `budget_s` seconds of oracle time have
-    been spent; the first pass also gives the parity of the GPU output on every sequence it
-    reaches."""
+def _oracle_worker(conn):
+    """One process of the oracle baseline pool.  Receives the directory holding the decode batch
+    (q, both pools, block table, context lengths as .npy files) and its share of the sequences,
+    copies those sequences' pages into private compact pools, reports ready, waits for the start
+    message with its time budget, then decodes its sequences in turn, passing over them again,
+    until the budget is spent.  Sends back the count, the keys attended, its elapsed time and the
+    outputs of its first pass (for the parity check)."""
+    try:
+        job = conn.recv()
+        if job is None:
+            return
+        import numpy as np
+        from threadpoolctl import threadpool_limits
+        import oracle
+        ld = lambda n: np.load(os.path.join(job["dir"], n + ".npy"), mmap_mode="r")
+        q, kp, vp, bt, ctx = ld("q"), ld("k_pool"), ld("v_pool"), ld("block_table"), ld("ctx_lens")
+        units = []
+        for b in job["seqs"]:
+            keys = int(ctx[b]) + 1
+            pages = np.asarray(bt[b, :(keys + 15) // 16])
+            units.append({"b": b, "q": np.array(q[b:b + 1]), "kp": np.array(kp[pages]), "vp": np.array(vp[pages]),
+                          "bt": np.arange(len(pages), dtype=np.int32)[None, :], "ctx": np.array(ctx[b:b + 1]),
+                          "keys": keys})
+        del q, kp, vp, bt, ctx
+        scale = job["scale"]
+        conn.send("ready")
+        budget = conn.recv()
+        if budget is None:
+            return
+        outs, done, keys, passes = {}, 0, 0, 0
+        with threadpool_limits(limits=1):
+            t0 = time.perf_counter()
+            while time.perf_counter() - t0 < budget:
+                for u in units:
+                    o, _ = oracle.attention(u["q"], u["kp"], u["vp"], u["bt"], u["ctx"], None, scale)
+                    done += 1
+                    keys += u["keys"]
+                    if passes == 0:
+                        outs[u["b"]] = o
+                    if time.perf_counter() - t0 >= budget:
+                        break
+                passes += 1
+            seconds = time.perf_counter() - t0
+        conn.send({"done": done, "keys": keys, "seconds": seconds, "outs": outs, "passes": passes})
+    except (EOFError, KeyboardInterrupt):
+        pass
+
+
+class OraclePool:
+    """Worker processes for the oracle baseline, started before this process touches the GPU
+    (spawned interpreters with one BLAS thread each, one per available core, at most 16)."""
+
+    def __init__(self, n):
+        import multiprocessing as mp
+        ctx = mp.get_context("spawn")
+        saved = {k: os.environ.get(k) for k in BLAS_THREAD_VARS}
+        for k in BLAS_THREAD_VARS:
+            os.environ[k] = "1"
+        self.procs, self.conns = [], []
+        try:
+            for _ in range(n):
+                a, b = ctx.Pipe()
+                p = ctx.Process(target=_oracle_worker, args=(b,), daemon=True)
+                p.start()
+                b.close()
+                self.procs.append(p)
+                self.conns.append(a)
+        finally:
+            for k, v in saved.items():
+                if v is None:
+                    os.environ.pop(k, None)
+                else:
+                    os.environ[k] = v
+
+    def run(self, data_dir, shares, scale, budget_s):
+        used = [c for c, sh in zip(self.conns, shares) if sh]
+        for c, sh in zip(self.conns, shares):
+            c.send({"dir": data_dir, "seqs": sh, "scale": scale} if sh else None)
+        for c in used:
+            assert c.recv() == "ready"
+        t0 = time.perf_counter()
+        for c in used:
+            c.send(budget_s)
+        res = [c.recv() for c in used]
+        wall = time.perf_counter() - t0
+        self.close()
+        return res, wall
+
+    def close(self):
+        for c in self.conns:
+            try:
+                c.close()
+            except Exception:
+                pass
+        for p in self.procs:
+            p.join(timeout=10)
+            if p.is_alive():
+                p.terminate()
+        self.procs, self.conns = [], []
+
+
+def _spill_dir(need):
+    """A fresh directory for the oracle's input files: in /dev/shm when it has room to spare, else
+    under the temporary directory.  Files are written with write(), so a full file system raises."""
+    import shutil
+    import tempfile
+    for base in ("/dev/shm", tempfile.gettempdir()):
+        try:
+            if os.path.isdir(base) and shutil.disk_usage(base).free > 2 * need:
+                return tempfile.mkdtemp(prefix="pearl_oracle_", dir=base)
+        except OSError:
+            pass
+    raise RuntimeError("no room for %d bytes of oracle inputs" % need)
+
+
+def cpu_baseline(torch, case, out, budget_s, pool):
+    """The oracle decoding the headline batch on this host: each worker of `pool` takes a share of
+    the sequences (random order, dealt round-robin) and decodes them, one sequence after another
+    and again, until `budget_s` seconds have passed.  value = sequences decoded / wall time.  The
+    workers' first passes give the parity of the GPU output on every sequence."""
+    import shutil
     import numpy as np
-    from threadpoolctl import threadpool_limits
     import oracle
     as_bits = lambda t: t.contiguous().view(torch.int16).cpu().numpy().view(np.uint16)
-    q_bits = as_bits(case.q)
     out_bits = as_bits(out)
-    done, t_total, passes = 0, 0.0, 0
-    keys = 0
+    arrays = {"q": as_bits(case.q), "k_pool": as_bits(case.k_pool), "v_pool": as_bits(case.v_pool),
+              "block_table": case.block_table.cpu().numpy(), "ctx_lens": case.ctx_lens.astype(np.int32)}
+    data_dir = _spill_dir(sum(a.nbytes for a in arrays.values()))
+    try:
+        for name, a in arrays.items():
+            with open(os.path.join(data_dir, name + ".npy"), "wb") as f:
+                np.save(f, a)
+        del arrays
+        n = len(pool.procs)
+        order = np.random.default_rng(123).permutation(case.batch)
+        shares = [[int(b) for b in order[i::n]] for i in range(n)]
+        res, wall = pool.run(data_dir, shares, case.scale, budget_s)
+    finally:
+        shutil.rmtree(data_dir, ignore_errors=True)
+    done = sum(r["done"] for r in res)
+    keys = sum(r["keys"] for r in res)
     errs = []
-    pools = {}
-    rng = np.random.default_rng(123)
-    order = rng.permutation(case.batch)
-    with threadpool_limits(limits=1):
-        while t_total < budget_s:
-            for b in order:
-                b = int(b)
-                if b not in pools:
-                    pools[b] = compact_pool(torch, case, [b])
-                kp, vp, sbt = pools[b]
-                t0 = time.perf_counter()
-                o, _ = oracle.attention(q_bits[b:b + 1], kp, vp, sbt, case.ctx_lens[b:b + 1], None, case.scale)
-                t_total += time.perf_counter() - t0
-                done += 1
-                keys += int(case.kv_lens[b])
-                if passes == 0:
-                    errs.append(oracle.compare(out_bits[b:b + 1], o))
-                if t_total >= budget_s:
-                    break
-            passes += 1
+    for r in res:
+        for b, o in r["outs"].items():
+            errs.append(oracle.compare(out_bits[b:b + 1], o))
+    used = len(res)
     return {
-        "value": done / t_total, "unit": "tok/s", "cores": 1, "kind": "oracle",
-        "sample": "%d sequence decodes (%d passes over the %d-sequence decode batch in random order, %d keys "
-                  "attended, all %d q-heads), numpy float64, 1 BLAS thread, %.1f s"
-                  % (done, passes, case.batch, keys, case.num_q_heads, t_total),
-        "cpu": cpu_model(),
+        "value": done / wall, "unit": "tok/s", "cores": used, "kind": "oracle",
+        "sample": "%d sequence decodes of the %d-sequence decode batch (%d keys attended, all %d q-heads) "
+                  "by %d worker processes, each with 1 BLAS thread, passing over its share of the batch "
+                  "until %.0f s had passed (%.1f s wall); numpy float64"
+                  % (done, case.batch, keys, case.num_q_heads, used, budget_s, wall),
+        "cpu": cpu_model(), "wall_s": round(wall, 2),
+        "per_core_tok_s": round(done / sum(r["seconds"] for r in res), 3),
     }, {
         "sequences": len(errs),
         "max_abs": max(e["max_abs"] for e in errs), "mean_abs": float(np.mean([e["mean_abs"] for e in errs])),
@@ -553,6 +765,25 @@ def measured_traffic(kernel, workload):
     return None
 
 
+def kernel_counters(kernel, workload):
+    """Clock, MFMA use and occupancy of a kernel from the committed rocprofv3 counter pass, or None
+    when no record exists or the kernel source changed since the counters were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "kernel_counters.json")
+    try:
+        data = json.load(open(path))
+    except Exception:
+        return None
+    for e in data.get("entries", []):
+        if e.get("kernel") == kernel and e.get("workload") == workload:
+            src = open(os.path.join(ROOT, e["source"]), "rb").read()
+            if hashlib.sha256(src).hexdigest() != e.get("source_sha256"):
+                return None
+            return {"sclk_mhz": e["sclk_mhz"], "mfma_busy": e["mfma_busy"], "waves_per_cu": e["waves_per_cu"],
+                    "mfma_bf16_flop": e["mfma_bf16_flop"], "from": "profiles/kernel_counters.json"}
+    return None
+
+
 def cpu_model():
     try:
         for line in open("/proc/cpuinfo"):
@@ -572,6 +803,8 @@ def main():
               "sequence and kv-head with no exchange; see the sharding notes). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
+    # the oracle's worker processes start before this process touches the GPU
+    pool = None if args.no_cpu else OraclePool(max(1, min(16, len(os.sched_getaffinity(0)))))
     import numpy as np
     import torch
     import paper_2609_35158_amd as pa
@@ -592,15 +825,24 @@ def main():
         del src, dst
         torch.cuda.empty_cache()
 
+    probe, flush, _flush_buf = hbm_probe(torch)
+    torch.cuda.empty_cache()
+    log("bench: measured HBM: read %.0f GB/s, write %.0f GB/s, copy %.0f GB/s"
+        % (probe["read_GBps"], probe["write_GBps"], probe["copy_GBps"]))
+
+    def vs_measured(gbps):
+        return {"read": round(gbps / probe["read_GBps"], 4), "copy": round(gbps / probe["copy_GBps"], 4)}
+
     # ---- headline: Qwen3-8B decode, B=64 -------------------------------------------------------
     log("bench: generating qwen3-8b decode (B=64, ctx U[2048,16384])")
     case = workloads.qwen3_8b_decode("cuda")
-    step, out = make_step(torch, pa, case, "decode")
-    step(lambda: None)             # first append
+    step, out, reps = make_rotating_step(torch, pa, case, "decode")
+    for _ in reps:
+        step(lambda: None)         # first append into every replica
     torch.cuda.synchronize()
-    ms_step, ms_kernel = run_timed(torch, pa, step, args.steps, args.warmup)
-    _, ms_app = time_append(torch, pa, step, args.steps)
-    ms_graph = time_graph_step(torch, pa, case, args.steps, args.warmup)
+    ms_step, ms_kernel, launches = run_timed(torch, pa, step, args.steps, args.warmup)
+    _, ms_app, _ = time_append(torch, pa, step, args.steps)
+    ms_graph = time_graph_step(torch, pa, reps, args.steps, args.warmup)
     nbytes = attn_bytes(case)
     flops = attn_flops(case)
     tok_s = case.batch / (ms_step * 1e-3)
@@ -628,28 +870,36 @@ def main():
             "num_q_heads": 32, "num_kv_heads": 8, "page_size": 16,
         },
         "hbm_tbps_step": round(nbytes / (ms_step * 1e-3) / 1e12, 4),
-        "roofline": {
+        "roofline": dict({
             "kernel": "attn_kernel<128, decode> (decode split items)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
             "traffic": measured_traffic("attn_kernel<128>", "qwen3-8b-decode-b64"),
             "algorithmic_bytes": nbytes, "kernel_ms": round(ms_kernel, 5),
+            "frac_of_measured": vs_measured(achieved),
             "tflops": round(flops / (ms_kernel * 1e-3) / 1e12, 2),
-        },
+            "counters": kernel_counters("attn_kernel<128>", "qwen3-8b-decode-b64"),
+        }, **launch_stats(launches)),
+        "timing": {"input_replicas": len(reps),
+                   "what": "consecutive steps use different copies of the inputs (others >= 1 GiB between two "
+                           "uses of one copy), so each step reads its K/V from HBM, not from L2 or the "
+                           "Infinity Cache; kernel times from HIP events around each launch"},
+        "hbm_measured": probe,
         "graph_step": {"ms_per_step": round(ms_graph, 5), "tok_s": round(case.batch / (ms_graph * 1e-3), 1),
-                       "what": "the same step captured once in a HIP graph and replayed"},
+                       "what": "the same steps captured once in a HIP graph (one per input copy) and replayed"},
         "kv_append": {"kernel_ms": round(ms_app, 5), "bytes": append_bytes(case),
                       "GBps": round(append_bytes(case) / (ms_app * 1e-3) / 1e9, 1)},
         "device": gpu_name,
     }
-    if not args.no_cpu:
-        log("bench: CPU oracle baseline (%.0f s budget)" % args.cpu_seconds)
-        cb, parity = cpu_baseline(torch, case, out, args.cpu_seconds)
+    del step, reps
+    if pool is not None:
+        log("bench: CPU oracle baseline (%d workers, %.0f s)" % (len(pool.procs), args.cpu_seconds))
+        cb, parity = cpu_baseline(torch, case, out, args.cpu_seconds, pool)
         result["cpu_baseline"] = cb
         result["parity_sample"] = parity
-        log("bench: cpu %.2f tok/s; parity on %d sequences max_abs %.2e mean_abs %.2e"
-            % (cb["value"], parity["sequences"], parity["max_abs"], parity["mean_abs"]))
-    del case, step, out
+        log("bench: cpu %.2f tok/s on %d cores; parity on %d sequences max_abs %.2e mean_abs %.2e"
+            % (cb["value"], cb["cores"], parity["sequences"], parity["max_abs"], parity["mean_abs"]))
+    del case, out
     torch.cuda.empty_cache()
 
     # ---- secondary workloads ------------------------------------------------------------------
@@ -668,44 +918,58 @@ def main():
                 continue
             log("bench: secondary %s" % name)
             c = gen()
-            st, o = make_step(torch, pa, c, mode)
-            st(lambda: None)
+            st, o, reps = make_rotating_step(torch, pa, c, mode)
+            for _ in reps:
+                st(lambda: None)
             torch.cuda.synchronize()
-            ms_s, ms_k = run_timed(torch, pa, st, args.steps, args.warmup)
-            _, ms_a = time_append(torch, pa, st, args.steps)
+            ms_s, ms_k, launches = run_timed(torch, pa, st, args.steps, args.warmup)
+            _, ms_a, _ = time_append(torch, pa, st, args.steps)
             b_ = attn_bytes(c)
             f_ = attn_flops(c)
-            entry = {"workload": name, "mode": mode, "ms_per_step": round(ms_s, 5), "kernel_ms": round(ms_k, 5),
-                     "batch": c.batch, "new_tokens": c.total_q, "keys": int(c.kv_lens.sum()),
-                     "algorithmic_bytes": b_, "flops": f_,
-                     "GBps": round(b_ / (ms_k * 1e-3) / 1e9, 1),
-                     "TFLOPs": round(f_ / (ms_k * 1e-3) / 1e12, 2),
-                     "kv_append_ms": round(ms_a, 5),
-                     "kv_append_GBps": round(append_bytes(c) / (ms_a * 1e-3) / 1e9, 1)}
+            entry = dict({"workload": name, "mode": mode, "ms_per_step": round(ms_s, 5), "kernel_ms": round(ms_k, 5)},
+                         **launch_stats(launches))
+            entry.update({"batch": c.batch, "new_tokens": c.total_q, "keys": int(c.kv_lens.sum()),
+                          "algorithmic_bytes": b_, "flops": f_,
+                          "GBps": round(b_ / (ms_k * 1e-3) / 1e9, 1),
+                          "TFLOPs": round(f_ / (ms_k * 1e-3) / 1e12, 2),
+                          "kv_append_ms": round(ms_a, 5),
+                          "kv_append_GBps": round(append_bytes(c) / (ms_a * 1e-3) / 1e9, 1),
+                          "input_replicas": len(reps)})
             if mode == "decode":
                 entry["tok_s"] = round(c.batch / (ms_s * 1e-3), 1)
                 entry["frac_hbm"] = round(entry["GBps"] / HBM_PEAK_GBPS, 4)
+                entry["frac_of_measured"] = vs_measured(entry["GBps"])
             elif mode == "prefill":
                 entry["frac_mfma"] = round(entry["TFLOPs"] / BF16_PEAK_TFLOPS, 4)
+                cnt = kernel_counters("attn_kernel<128>", name)
+                entry["counters"] = cnt
+                if cnt:
+                    # the published peak is quoted at 2400 MHz; the same MFMA units at the clock the
+                    # counters measured over this kernel
+                    peak_at = BF16_PEAK_TFLOPS * cnt["sclk_mhz"] / 2400.0
+                    entry["mfma_peak_at_measured_sclk_TFLOPs"] = round(peak_at, 1)
+                    entry["frac_mfma_at_measured_sclk"] = round(entry["TFLOPs"] / peak_at, 4)
             else:
                 t_hbm = b_ / (HBM_PEAK_GBPS * 1e9) * 1e3
                 t_mfma = f_ / (BF16_PEAK_TFLOPS * 1e12) * 1e3
                 entry["roofline_ms_overlapped"] = round(max(t_hbm, t_mfma), 4)
                 entry["roofline_ms_serial"] = round(t_hbm + t_mfma, 4)
                 entry["frac_of_overlapped_bound"] = round(max(t_hbm, t_mfma) / ms_k, 4)
+                t_hbm_m = b_ / (probe["read_GBps"] * 1e9) * 1e3
+                entry["frac_of_overlapped_bound_measured_hbm"] = round(max(t_hbm_m, t_mfma) / ms_k, 4)
             log("bench:   %s" % json.dumps(entry))
             sec.append(entry)
-            del c, st, o
+            del c, st, o, reps
             torch.cuda.empty_cache()
         if not only or "kv-transfer" in only:
             log("bench: secondary kv-transfer")
-            sec.extend(kv_transfer(torch, pa, workloads, args.steps, args.warmup))
+            sec.extend(kv_transfer(torch, pa, workloads, args.steps, args.warmup, flush))
         if not only or "pd-engine" in only:
             log("bench: secondary pd-engine")
-            sec.append(pd_engine(torch, pa, workloads, max(5, args.steps // 2), args.warmup))
+            sec.append(pd_engine(torch, pa, workloads, max(5, args.steps // 2), args.warmup, flush))
         if not only or "pd-interference" in only:
             log("bench: secondary pd-interference")
-            sec.append(pd_interference(torch, pa, workloads, max(5, args.steps // 2), args.warmup))
+            sec.append(pd_interference(torch, pa, workloads, max(5, args.steps // 2), args.warmup, flush))
         result["secondary"] = sec
     print(json.dumps(result), flush=True)
 

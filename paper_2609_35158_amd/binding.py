@@ -41,7 +41,8 @@ class SeqDesc(ctypes.Structure):
 
 EXPORTED = ("pearl_abi_version", "pearl_status_str", "pearl_last_error", "pearl_kv_append",
             "pearl_attn_workspace_bytes", "pearl_attn_prefill_append", "pearl_attn_decode",
-            "pearl_attn_mixed", "pearl_kv_pack", "pearl_kv_unpack", "pearl_set_kernel_events")
+            "pearl_attn_mixed", "pearl_kv_pack", "pearl_kv_unpack", "pearl_set_kernel_events",
+            "pearl_hbm_copy", "pearl_hbm_read", "pearl_hbm_fill")
 
 
 def load(path: str = LIB_PATH):
@@ -78,6 +79,13 @@ def load(path: str = LIB_PATH):
                       ctypes.c_size_t, ctypes.c_void_p]
     lib.pearl_set_kernel_events.restype = None
     lib.pearl_set_kernel_events.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+    # measurement tooling (include/pearl_bench.h)
+    lib.pearl_hbm_copy.restype = ctypes.c_int
+    lib.pearl_hbm_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
+    lib.pearl_hbm_read.restype = ctypes.c_int
+    lib.pearl_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    lib.pearl_hbm_fill.restype = ctypes.c_int
+    lib.pearl_hbm_fill.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32, ctypes.c_void_p]
     _lib = lib
     return lib
 
@@ -263,3 +271,34 @@ def mixed(q, k_pool, v_pool, block_table, ctx_lens, cu_q_lens, max_q_len, max_kv
     """Colocated prefill chunks and decodes in one attention launch (pearl_attn_mixed)."""
     return _attention("pearl_attn_mixed", q, k_pool, v_pool, block_table, ctx_lens, cu_q_lens,
                       max_q_len, max_kv_len, scale, return_lse, out, lse, workspace)
+
+
+# ------------------------------------------------------------------------------------------------
+# measurement tooling (include/pearl_bench.h): bandwidth probes and the cache flush
+# ------------------------------------------------------------------------------------------------
+
+def hbm_copy(src: torch.Tensor, dst: torch.Tensor) -> None:
+    """dst <- src, byte for byte (both contiguous GPU tensors of the same byte size)."""
+    if not (src.is_cuda and dst.is_cuda and src.is_contiguous() and dst.is_contiguous()):
+        raise ValueError("hbm_copy needs contiguous GPU tensors")
+    n = src.numel() * src.element_size()
+    if dst.numel() * dst.element_size() != n:
+        raise ValueError("hbm_copy: byte sizes differ")
+    _check(load().pearl_hbm_copy(src.data_ptr(), dst.data_ptr(), n, _stream()), "pearl_hbm_copy")
+
+
+def hbm_read(src: torch.Tensor, sink: torch.Tensor) -> None:
+    """Stream-read src; `sink` is a 16-byte (or larger) GPU tensor the kernel may overwrite.  Over
+    >= 1 GiB this is the cache flush (it leaves no dirty lines behind)."""
+    if not (src.is_cuda and src.is_contiguous() and sink.is_cuda and sink.numel() * sink.element_size() >= 16):
+        raise ValueError("hbm_read needs a contiguous GPU source and a 16-byte GPU sink")
+    _check(load().pearl_hbm_read(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(), _stream()),
+           "pearl_hbm_read")
+
+
+def hbm_fill(dst: torch.Tensor, pattern: int = 0) -> None:
+    """Write a 32-bit pattern over dst."""
+    if not (dst.is_cuda and dst.is_contiguous()):
+        raise ValueError("hbm_fill needs a contiguous GPU tensor")
+    _check(load().pearl_hbm_fill(dst.data_ptr(), dst.numel() * dst.element_size(), pattern & 0xFFFFFFFF,
+                                 _stream()), "pearl_hbm_fill")

@@ -12,7 +12,7 @@ PKG = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 LIB = os.path.join(PKG, "libpearl_attn.so")
-SOURCES = ["attn_kernels.hip", "kv_pages.hip", "api.cpp", "pd_engine.cpp"]
+SOURCES = ["attn_kernels.hip", "kv_pages.hip", "hbm_probe.hip", "api.cpp", "pd_engine.cpp"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

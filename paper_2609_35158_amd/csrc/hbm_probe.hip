@@ -1,0 +1,108 @@
+// Measurement tooling, not part of the attention computation: plain streaming kernels that
+// give the HBM bandwidth this device actually reaches (copy, read-only, write-only); a read-only
+// pass over a large scratch buffer is the cache flush (it replaces the contents of the L2 caches
+// and of the memory-side Infinity Cache with clean lines).  Benchmarks use them to state kernel
+// times against measured, not only published, bandwidth and to start timed launches with cold
+// caches.
+//
+// Each workgroup streams one contiguous span of kSpan 16-byte vectors; thread t handles vectors
+// t, t + 256, ..., so every load and store instruction of a wave covers 1 KiB of consecutive
+// bytes, and all kUnroll loads of a thread are in flight before its first store.
+
+#include "pearl_internal.h"
+#include "../../include/pearl_bench.h"
+
+namespace pearl {
+
+typedef unsigned int v4u __attribute__((ext_vector_type(4)));
+
+constexpr int kProbeThreads = 256;
+constexpr int kProbeUnroll = 8;
+constexpr size_t kSpan = (size_t)kProbeThreads * kProbeUnroll;   // vectors per workgroup
+
+enum ProbeMode : int { kProbeCopy = 0, kProbeRead = 1, kProbeFill = 2 };
+
+template <int kMode>
+__global__ __launch_bounds__(kProbeThreads) void hbm_stream_kernel(const v4u* __restrict__ src,
+                                                                   v4u* __restrict__ dst, size_t n,
+                                                                   v4u key) {
+  const size_t base = (size_t)blockIdx.x * kSpan + threadIdx.x;
+  if (kMode == kProbeFill) {
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+      const size_t i = base + (size_t)u * kProbeThreads;
+      if (i < n) dst[i] = key;
+    }
+    return;
+  }
+  v4u x[kProbeUnroll];
+#pragma unroll
+  for (int u = 0; u < kProbeUnroll; ++u) {
+    const size_t i = base + (size_t)u * kProbeThreads;
+    x[u] = i < n ? src[i] : v4u{0u, 0u, 0u, 0u};
+  }
+  if (kMode == kProbeCopy) {
+#pragma unroll
+    for (int u = 0; u < kProbeUnroll; ++u) {
+      const size_t i = base + (size_t)u * kProbeThreads;
+      if (i < n) dst[i] = x[u];
+    }
+  } else {
+    // read-only: fold the loaded words so the loads cannot be dropped, and store the fold only
+    // when it equals the caller's key (in practice never; the sink is a valid 16-byte slot).
+    v4u acc = x[0];
+#pragma unroll
+    for (int u = 1; u < kProbeUnroll; ++u) acc ^= x[u];
+    if (acc.x == key.x && acc.y == key.y && acc.z == key.z && acc.w == key.w) dst[0] = acc;
+  }
+}
+
+namespace {
+
+pearl_status launch_probe(int mode, const void* src, void* dst, size_t bytes, uint32_t pattern,
+                          void* stream, const char* fn) {
+  clear_error();
+  if (bytes == 0) return PEARL_OK;
+  if (bytes % 16 != 0) return set_error(PEARL_ERR_INVALID_ARG, "%s: bytes (%zu) is not a multiple of 16", fn, bytes);
+  if ((mode != kProbeFill && src == nullptr) || dst == nullptr)
+    return set_error(PEARL_ERR_INVALID_ARG, "%s: null buffer", fn);
+  if (((uintptr_t)src | (uintptr_t)dst) % 16 != 0)
+    return set_error(PEARL_ERR_INVALID_ARG, "%s: buffers must be 16-byte aligned", fn);
+  const size_t n = bytes / 16;
+  const size_t blocks = (n + kSpan - 1) / kSpan;
+  if (blocks > 0x7fffffffull) return set_error(PEARL_ERR_UNSUPPORTED, "%s: %zu bytes is too large", fn, bytes);
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const v4u key{pattern, pattern, pattern, pattern};
+  const v4u* in = reinterpret_cast<const v4u*>(src);
+  v4u* out = reinterpret_cast<v4u*>(dst);
+  const dim3 grid((unsigned)blocks), block(kProbeThreads);
+  if (mode == kProbeCopy)
+    hipLaunchKernelGGL(hbm_stream_kernel<kProbeCopy>, grid, block, 0, s, in, out, n, key);
+  else if (mode == kProbeRead)
+    hipLaunchKernelGGL(hbm_stream_kernel<kProbeRead>, grid, block, 0, s, in, out, n, key);
+  else
+    hipLaunchKernelGGL(hbm_stream_kernel<kProbeFill>, grid, block, 0, s, in, out, n, key);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return set_error(PEARL_ERR_HIP, "%s: launch failed: %s", fn, hipGetErrorString(e));
+  return PEARL_OK;
+}
+
+}  // namespace
+}  // namespace pearl
+
+extern "C" {
+
+pearl_status pearl_hbm_copy(const void* src, void* dst, size_t bytes, void* stream) {
+  return pearl::launch_probe(pearl::kProbeCopy, src, dst, bytes, 0u, stream, "pearl_hbm_copy");
+}
+
+pearl_status pearl_hbm_read(const void* src, size_t bytes, void* sink, void* stream) {
+  // the key is a value a fold of real data essentially never takes; a match only writes the sink
+  return pearl::launch_probe(pearl::kProbeRead, src, sink, bytes, 0x9e3779b9u, stream, "pearl_hbm_read");
+}
+
+pearl_status pearl_hbm_fill(void* dst, size_t bytes, uint32_t pattern, void* stream) {
+  return pearl::launch_probe(pearl::kProbeFill, nullptr, dst, bytes, pattern, stream, "pearl_hbm_fill");
+}
+
+}  // extern "C"

@@ -138,3 +138,19 @@ def test_python_layer_refuses_cpu_tensors():
     with pytest.raises((ValueError, TypeError)):
         pa.decode(q, q.view(2, 1, 4, 64), q.view(2, 1, 4, 64), torch.zeros(2, 1, dtype=torch.int32),
                   torch.zeros(2, dtype=torch.int32), 1)
+
+
+def test_hbm_probe_host_validation():
+    """The measurement kernels of include/pearl_bench.h reject bad arguments before any HIP call
+    and do nothing for zero bytes."""
+    lib = pa.load()
+    assert lib.pearl_hbm_copy(FAKE, FAKE + 4096, 0, None) == 0
+    assert lib.pearl_hbm_fill(FAKE, 0, 7, None) == 0
+    assert lib.pearl_hbm_copy(FAKE, FAKE + 4096, 24, None) == INVALID and "multiple of 16" in pa.last_error()
+    assert lib.pearl_hbm_copy(None, FAKE, 32, None) == INVALID and "null" in pa.last_error()
+    assert lib.pearl_hbm_copy(FAKE, None, 32, None) == INVALID
+    assert lib.pearl_hbm_read(FAKE + 8, 32, FAKE, None) == INVALID and "aligned" in pa.last_error()
+    assert lib.pearl_hbm_read(FAKE, 32, FAKE + 4, None) == INVALID and "aligned" in pa.last_error()
+    assert lib.pearl_hbm_read(FAKE, 32, None, None) == INVALID
+    assert lib.pearl_hbm_fill(None, 32, 0, None) == INVALID
+    assert lib.pearl_hbm_fill(FAKE, 40, 0, None) == INVALID
