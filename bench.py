@@ -16,7 +16,8 @@ The same line carries:
                 committed rocprofv3 counter pass (while the kernel source is unchanged);
   cpu_baseline  the CPU oracle (numpy float64) timed on this host by a pool of single-threaded
                 worker processes, one per core, on a bounded sample;
-  secondary     prefill-append TFLOP/s (Qwen3-8B shape), Qwen3-30B-A3B-shaped decode at batch
+  secondary     prefill-append TFLOP/s (Qwen3-8B shape), the headline decode's per-GPU share under
+                tensor parallelism 2 (16 q-heads, 4 kv-heads), Qwen3-30B-A3B-shaped decode at batch
                 256/128/32, the colocated mixed batch, kv_append GB/s, KV transfer pack/unpack
                 GB/s, a decode/prefill interference sweep (one mixed launch vs decode alone
                 as prefill chunks grow), and the PD decision engine calibrated from the kernels.
@@ -908,6 +909,8 @@ def main():
         only = set(x for x in args.only.split(",") if x)
         specs = [
             ("qwen3-8b-prefill-append", "prefill", lambda: workloads.qwen3_8b_prefill_append("cuda"), "mfma"),
+            ("qwen3-8b-decode-b64-tp2-shard", "decode",
+             lambda: workloads.qwen3_8b_decode("cuda", num_q_heads=16, num_kv_heads=4), "hbm"),
             ("qwen3-30b-a3b-decode-b256", "decode", lambda: workloads.qwen3_30b_decode("cuda", batch=256), "hbm"),
             ("qwen3-30b-a3b-decode-b128", "decode", lambda: workloads.qwen3_30b_decode("cuda", batch=128), "hbm"),
             ("qwen3-30b-a3b-decode-b32", "decode", lambda: workloads.qwen3_30b_decode("cuda", batch=32), "hbm"),

@@ -200,12 +200,17 @@ def tiny_prefill(device="cpu") -> Case:
     return full
 
 
-def qwen3_8b_decode(device="cpu", batch=64, seed=1, lo=2048, hi=16384) -> Case:
+def qwen3_8b_decode(device="cpu", batch=64, seed=1, lo=2048, hi=16384, num_q_heads=32,
+                    num_kv_heads=8) -> Case:
     """Qwen3-8B attention shape (32 q-heads, 8 kv-heads, d=128); `batch` sequences with cached
-    contexts uniform in [lo, hi]; one new token each; pool sized to the total context."""
+    contexts uniform in [lo, hi]; one new token each; pool sized to the total context.  With
+    16 q-heads and 4 kv-heads it is one GPU's share under tensor parallelism 2 (same lengths and
+    page placement)."""
     rng = np.random.default_rng(seed + 1_000_003)
     ctx = rng.integers(lo, hi, size=batch, endpoint=True)
-    return build_case("qwen3-8b-decode", seed, 32, 8, 128, ctx, np.ones(batch, np.int64), device=device)
+    name = "qwen3-8b-decode" if (num_q_heads, num_kv_heads) == (32, 8) else \
+        "qwen3-8b-decode-h%d-%d" % (num_q_heads, num_kv_heads)
+    return build_case(name, seed, num_q_heads, num_kv_heads, 128, ctx, np.ones(batch, np.int64), device=device)
 
 
 def qwen3_8b_prefill_append(device="cpu", batch=16, seed=2, ctx_lo=4096, ctx_hi=24576,
