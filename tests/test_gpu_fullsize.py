@@ -42,10 +42,12 @@ def _appended_rows_match(case, seqs):
             assert np.array_equal(got, bits(case.k_new[cu[b] + t])), (b, t)
 
 
-@pytest.mark.parametrize("batch", [64])
-def test_qwen3_8b_decode_fullsize(batch):
-    say("case: qwen3-8b decode B=%d full size" % batch)
-    case = workloads.qwen3_8b_decode("cuda", batch=batch)
+@pytest.mark.parametrize("heads", [(32, 8), (16, 4)])
+def test_qwen3_8b_decode_fullsize(heads):
+    """The headline batch, and one GPU's share of it under tensor parallelism 2 (half the heads)."""
+    batch = 64
+    say("case: qwen3-8b decode B=%d heads %s full size" % (batch, heads))
+    case = workloads.qwen3_8b_decode("cuda", batch=batch, num_q_heads=heads[0], num_kv_heads=heads[1])
     gpu_append(case)
     out, lse = gpu_attend(case, "decode")
     torch.cuda.synchronize()
