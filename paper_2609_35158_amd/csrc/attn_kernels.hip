@@ -125,7 +125,17 @@ template <int D, int NW, int kKinds> struct Lds {
 // split.  S is at least kMinSplitKeys and at least the tile keys per unit, which keeps the split
 // items of a launch under 2 * kPlanComputeUnits (the partial-slot capacity).
 // ------------------------------------------------------------------------------------------------
-constexpr int kPlanThreads = 1024;
+constexpr int kPlanThreads = 256;
+// Decode splits are ordered longest first: every full split (pages_per_split pages), then each
+// sequence's shorter last split in kPartBuckets size classes, largest class first, so the last
+// items a launch hands out are its shortest ones.
+constexpr int kPartBuckets = 16;
+
+// Size class of a short last split of `rest` pages (1 <= rest < pps); class 0 holds the longest.
+// inv_pps = kPartBuckets / pps; the class only orders work, so rounding at a class edge is harmless.
+__device__ __forceinline__ int part_bucket(int rest, float inv_pps) {
+  return kPartBuckets - 1 - min(kPartBuckets - 1, (int)((float)(rest - 1) * inv_pps));
+}
 
 __device__ __forceinline__ int tile_splits(int ctx, int t0, int split_keys) {
   return split_keys > 0 ? (ctx + t0 + split_keys) / split_keys : 1;   // ceil((ctx + t0 + 1) / S)
@@ -137,19 +147,25 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     int2* __restrict__ entries, int4* __restrict__ pre_jobs) {
   __shared__ int s_err, s_tiles, s_max_full, s_split_keys, s_pre_first;
   __shared__ unsigned long long s_pre_keys, s_dec_keys;
-  __shared__ int s_wave[3][kPlanThreads / 64];
-  __shared__ int s_carry[3];
+  __shared__ int s_wave[4][kPlanThreads / 64];
+  __shared__ int s_carry[4];
+  __shared__ int s_n_full;                     // full decode splits of the launch
+  __shared__ int s_part_cnt[kPartBuckets];     // short last splits per size class, then fill counts
+  __shared__ int s_part_off[kPartBuckets];     // first position of each size class after the full splits
   const int tid = threadIdx.x;
   const int T = p.tokens_per_tile;
+  const int pps = p.pages_per_split;
+  const float inv_pps = (float)kPartBuckets / (float)pps;
   if (tid == 0) {
-    s_err = 0; s_tiles = 0; s_max_full = 0; s_pre_keys = 0; s_dec_keys = 0;
-    s_carry[0] = s_carry[1] = s_carry[2] = 0;
+    s_err = 0; s_tiles = 0; s_max_full = 0; s_pre_keys = 0; s_dec_keys = 0; s_n_full = 0;
+    s_carry[0] = s_carry[1] = s_carry[2] = s_carry[3] = 0;
   }
+  if (tid < kPartBuckets) s_part_cnt[tid] = 0;
   if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
   __syncthreads();
   // pass 1: validate every sequence and total the work
   {
-    int tiles = 0, max_full = 0;
+    int tiles = 0, max_full = 0, n_full = 0;
     unsigned long long pre_keys = 0, dec_keys = 0;
     for (int b = tid; b < p.batch; b += kPlanThreads) {
       const int q_start = cu ? cu[b] : b;
@@ -164,6 +180,10 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       if (q_len <= 0) continue;
       if (p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1)) {
         dec_keys += (unsigned long long)kv;
+        const int pages = (int)((kv + kPage - 1) / kPage);
+        const int rest = pages % pps;
+        n_full += pages / pps;
+        if (rest) atomicAdd(&s_part_cnt[part_bucket(rest, inv_pps)], 1);
       } else {
         const int nt = (q_len + T - 1) / T;
         tiles += nt;
@@ -173,6 +193,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       }
     }
     if (tiles) atomicAdd(&s_tiles, tiles);
+    if (n_full) atomicAdd(&s_n_full, n_full);
     if (max_full) atomicMax(&s_max_full, max_full);
     if (pre_keys) atomicAdd(&s_pre_keys, pre_keys);
     if (dec_keys) atomicAdd(&s_dec_keys, dec_keys);
@@ -211,14 +232,21 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
     s_pre_first = pre_first;
   }
+  if (tid < kPartBuckets) {                   // size classes, largest first, after the full splits
+    int off = s_n_full;
+    for (int k = 0; k < tid; ++k) off += s_part_cnt[k];
+    s_part_off[tid] = off;
+  }
+  __syncthreads();
+  if (tid < kPartBuckets) s_part_cnt[tid] = 0;   // now the fill count of each class
   __syncthreads();
   const int S = s_split_keys;
   // pass 2: per-sequence counts (prefill entries, decode entries, split tiles), block-wide
   // exclusive scans, then the entries: prefill tiles last (longest) tile first, splits in order
   for (int base = 0; base < p.batch; base += kPlanThreads) {
     const int b = base + tid;
-    int cnt[3] = {0, 0, 0};
-    int kind = kSeqNone, q_start = 0, q_len = 0, ctx = 0, nt = 0;
+    int cnt[4] = {0, 0, 0, 0};              // prefill entries, decode splits, split tiles, full decode splits
+    int kind = kSeqNone, q_start = 0, q_len = 0, ctx = 0, nt = 0, rest = 0;
     if (b < p.batch) {
       q_start = cu ? cu[b] : b;
       q_len = cu ? cu[b + 1] - q_start : 1;
@@ -228,7 +256,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         if (dec) {
           const int pages = (ctx + q_len + kPage - 1) / kPage;
           kind = kSeqDecode;
-          cnt[1] = (pages + p.pages_per_split - 1) / p.pages_per_split;
+          cnt[1] = (pages + pps - 1) / pps;
+          cnt[3] = pages / pps;
+          rest = pages - cnt[3] * pps;
         } else {
           kind = kSeqPrefill;
           nt = (q_len + T - 1) / T;
@@ -242,23 +272,23 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
     // exclusive scan: wave-level inclusive scans by shuffles, then the totals of earlier waves
     const int lane = tid & 63, wv = tid >> 6;
-    int incl[3] = {cnt[0], cnt[1], cnt[2]};
+    int incl[4] = {cnt[0], cnt[1], cnt[2], cnt[3]};
 #pragma unroll
     for (int off = 1; off < 64; off <<= 1) {
 #pragma unroll
-      for (int c = 0; c < 3; ++c) {
+      for (int c = 0; c < 4; ++c) {
         const int v = __shfl_up(incl[c], off);
         if (lane >= off) incl[c] += v;
       }
     }
     if (lane == 63) {
 #pragma unroll
-      for (int c = 0; c < 3; ++c) s_wave[c][wv] = incl[c];
+      for (int c = 0; c < 4; ++c) s_wave[c][wv] = incl[c];
     }
     __syncthreads();
-    int excl[3];
+    int excl[4];
 #pragma unroll
-    for (int c = 0; c < 3; ++c) {
+    for (int c = 0; c < 4; ++c) {
       int before = s_carry[c];
       for (int k = 0; k < wv; ++k) before += s_wave[c][k];
       excl[c] = before + incl[c] - cnt[c];
@@ -273,13 +303,22 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
         for (int sp = 0; sp < ns; ++sp, ++e)
           if (e < p.max_pre) entries[e] = make_int2(b, t | (sp << 16));
       }
-      for (int sp = 0; sp < cnt[1]; ++sp)
-        if (excl[1] + sp < p.max_dec) entries[p.max_pre + excl[1] + sp] = make_int2(b, sp);
+      // full splits in sequence order; the short last split at its size class's next position
+      // (claimed before the loop, so the wave issues the atomic once)
+      int part_pos = 0;
+      if (rest) {
+        const int k = part_bucket(rest, inv_pps);
+        part_pos = s_part_off[k] + atomicAdd(&s_part_cnt[k], 1);
+      }
+      for (int sp = 0; sp < cnt[1]; ++sp) {
+        const int pos = sp < cnt[3] ? excl[3] + sp : part_pos;
+        if (pos < p.max_dec) entries[p.max_pre + pos] = make_int2(b, sp);
+      }
     }
     __syncthreads();
     if (tid == kPlanThreads - 1) {
 #pragma unroll
-      for (int c = 0; c < 3; ++c) s_carry[c] = excl[c] + cnt[c];
+      for (int c = 0; c < 4; ++c) s_carry[c] = excl[c] + cnt[c];
     }
     __syncthreads();
   }
