@@ -596,6 +596,7 @@ def _oracle_worker(conn):
     until the budget is spent.  Sends back the count, the keys attended, its elapsed time and the
     outputs of its first pass (for the parity check)."""
     try:
+        conn.send("up")
         job = conn.recv()
         if job is None:
             return
@@ -638,7 +639,8 @@ def _oracle_worker(conn):
 
 class OraclePool:
     """Worker processes for the oracle baseline, started before this process touches the GPU
-    (spawned interpreters with one BLAS thread each, one per available core, at most 16)."""
+    (spawned interpreters with one BLAS thread each, one per available core, at most 16).  The
+    constructor returns once every worker is up, so their start-up cannot overlap GPU timing."""
 
     def __init__(self, n):
         import multiprocessing as mp
@@ -661,6 +663,8 @@ class OraclePool:
                     os.environ.pop(k, None)
                 else:
                     os.environ[k] = v
+        for c in self.conns:          # every interpreter has started before any GPU timing
+            assert c.recv() == "up"
 
     def run(self, data_dir, shares, scale, budget_s):
         used = [c for c, sh in zip(self.conns, shares) if sh]

@@ -175,7 +175,6 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   a.num_kv_heads = s->num_kv_heads;
   a.group = pl.p.group;
   a.tokens_per_tile = pl.p.tokens_per_tile;
-  a.pages_per_split = pl.p.pages_per_split;
   a.scale_log2 = scale * 1.4426950408889634f;
   const int64_t max_items = (pl.lay.max_pre + pl.lay.max_dec) * s->num_kv_heads;
   e = record_before(hs);
@@ -218,9 +217,10 @@ pearl_status set_error(pearl_status st, const char* fmt, ...) {
 }
 
 int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu) {
-  // Aim for about 16 decode items per compute unit when every sequence is as long as the bound;
-  // a split never holds fewer than 16 pages (one page pair for each of the 8 waves), and its size
-  // is a multiple of 16 pages.
+  // The least pages per decode split, which sizes the workspace: about 16 decode items per
+  // compute unit if every sequence were as long as the bound.  A split never holds fewer than 16
+  // pages (one page pair for each of the 8 waves), and its size is a multiple of 16 pages.  The
+  // planner takes larger splits from the launch's actual pages (kDecItemsPerCU).
   const int64_t max_pages = std::max<int64_t>(1, cdiv(std::max(max_kv_len, 1), kPage));
   const int64_t target = std::max<int64_t>(1, (int64_t)num_cu * 16);
   int64_t pps = cdiv((int64_t)batch * num_kv_heads * max_pages, target);

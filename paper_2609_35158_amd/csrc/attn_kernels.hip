@@ -150,23 +150,24 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __shared__ int s_wave[4][kPlanThreads / 64];
   __shared__ int s_carry[4];
   __shared__ int s_n_full;                     // full decode splits of the launch
+  __shared__ int s_pps;                        // pages per decode split
+  __shared__ unsigned long long s_dec_pages;
   __shared__ int s_part_cnt[kPartBuckets];     // short last splits per size class, then fill counts
   __shared__ int s_part_off[kPartBuckets];     // first position of each size class after the full splits
   const int tid = threadIdx.x;
   const int T = p.tokens_per_tile;
-  const int pps = p.pages_per_split;
-  const float inv_pps = (float)kPartBuckets / (float)pps;
   if (tid == 0) {
-    s_err = 0; s_tiles = 0; s_max_full = 0; s_pre_keys = 0; s_dec_keys = 0; s_n_full = 0;
+    s_err = 0; s_tiles = 0; s_max_full = 0; s_pre_keys = 0; s_dec_keys = 0; s_n_full = 0; s_dec_pages = 0;
     s_carry[0] = s_carry[1] = s_carry[2] = s_carry[3] = 0;
   }
   if (tid < kPartBuckets) s_part_cnt[tid] = 0;
   if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
   __syncthreads();
   // pass 1: validate every sequence and total the work
+  int my_pages = 0;                            // decode pages of sequence tid (first chunk)
   {
-    int tiles = 0, max_full = 0, n_full = 0;
-    unsigned long long pre_keys = 0, dec_keys = 0;
+    int tiles = 0, max_full = 0;
+    unsigned long long pre_keys = 0, dec_keys = 0, dec_pages = 0;
     for (int b = tid; b < p.batch; b += kPlanThreads) {
       const int q_start = cu ? cu[b] : b;
       const int q_len = cu ? cu[b + 1] - q_start : 1;
@@ -181,9 +182,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       if (p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1)) {
         dec_keys += (unsigned long long)kv;
         const int pages = (int)((kv + kPage - 1) / kPage);
-        const int rest = pages % pps;
-        n_full += pages / pps;
-        if (rest) atomicAdd(&s_part_cnt[part_bucket(rest, inv_pps)], 1);
+        dec_pages += (unsigned long long)pages;
+        if (b == tid) my_pages = pages;
       } else {
         const int nt = (q_len + T - 1) / T;
         tiles += nt;
@@ -193,7 +193,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       }
     }
     if (tiles) atomicAdd(&s_tiles, tiles);
-    if (n_full) atomicAdd(&s_n_full, n_full);
+    if (dec_pages) atomicAdd(&s_dec_pages, dec_pages);
     if (max_full) atomicMax(&s_max_full, max_full);
     if (pre_keys) atomicAdd(&s_pre_keys, pre_keys);
     if (dec_keys) atomicAdd(&s_dec_keys, dec_keys);
@@ -203,6 +203,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     if (tid == 0) {
       hdr[kHdrCounter] = 0; hdr[kHdrCounterPre] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
       hdr[kHdrError] = 1; hdr[kHdrNumItems] = 0; hdr[kHdrPreSplitKeys] = 0; hdr[kHdrNumPreJobs] = 0;
+      hdr[kHdrPagesPerSplit] = p.pages_per_split;
     }
     return;
   }
@@ -231,7 +232,40 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
                               : p.mixed_grid;
     }
     s_pre_first = pre_first;
+    // Decode split size: about kDecItemsPerCU items per compute unit over the launch's actual
+    // pages, a multiple of 16 pages, at least the host's bound and at most kMaxPagesPerSplit.
+    long long pps = p.pages_per_split;
+    if (s_dec_pages > 0) {
+      const long long per = (long long)kPlanComputeUnits * kDecItemsPerCU;
+      const long long want = ((long long)s_dec_pages * H + per - 1) / per;
+      pps = max(pps, (want + 15) / 16 * 16);
+      pps = min(pps, (long long)max(p.pages_per_split, kMaxPagesPerSplit));
+    }
+    s_pps = (int)pps;
   }
+  __syncthreads();
+  const int pps = s_pps;
+  const float inv_pps = (float)kPartBuckets / (float)pps;
+  // pass 1b: full decode splits and the size classes of the short last splits
+  {
+    int n_full = 0;
+    for (int b = tid; b < p.batch; b += kPlanThreads) {
+      int pages = my_pages;
+      if (b != tid) {
+        const int q_start = cu ? cu[b] : b;
+        const int q_len = cu ? cu[b + 1] - q_start : 1;
+        const bool dec = p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1);
+        pages = dec ? (ctx_lens[b] + q_len + kPage - 1) / kPage : 0;
+      }
+      if (pages > 0) {
+        const int rest = pages % pps;
+        n_full += pages / pps;
+        if (rest) atomicAdd(&s_part_cnt[part_bucket(rest, inv_pps)], 1);
+      }
+    }
+    if (n_full) atomicAdd(&s_n_full, n_full);
+  }
+  __syncthreads();
   if (tid < kPartBuckets) {                   // size classes, largest first, after the full splits
     int off = s_n_full;
     for (int k = 0; k < tid; ++k) off += s_part_cnt[k];
@@ -335,6 +369,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     hdr[kHdrNumItems] = over ? 0 : (n_pre + n_dec) * p.num_kv_heads;
     hdr[kHdrPreSplitKeys] = S;
     hdr[kHdrNumPreJobs] = over ? 0 : n_jobs;
+    hdr[kHdrPagesPerSplit] = pps;
   }
 }
 
@@ -819,7 +854,8 @@ __device__ __forceinline__ void decode_step(const AttnArgs& a, const PairPages& 
 }
 
 template <int D, int NW>
-__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, char* vbufA, char* vbufB) {
+__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, int pps, char* vbufA,
+                                             char* vbufB) {
   constexpr int NT = NW * 64;
   using VT = VTile<D>;
   constexpr int MB = D / 16;
@@ -831,8 +867,8 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
   const int G = a.group, H_q = a.num_q_heads;
   const int kv = si.ctx_len + si.q_len;
   const int n_pages = (kv + kPage - 1) / kPage;
-  const int p_begin = split * a.pages_per_split;
-  const int p_end = min(p_begin + a.pages_per_split, n_pages);
+  const int p_begin = split * pps;
+  const int p_end = min(p_begin + pps, n_pages);
   const int n_pairs = (p_end - p_begin + 1) / 2;
   const bool head_ok = hh < G;
   char* vb0 = vbufA + w * VT::PAIR_BYTES;
@@ -941,6 +977,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   const int n_items = a.ws_hdr[kHdrNumItems];
   const int n_pre = a.ws_hdr[kHdrNumPre];
   const int split_keys = a.ws_hdr[kHdrPreSplitKeys];
+  const int pps = a.ws_hdr[kHdrPagesPerSplit];
   const int H_kv = a.num_kv_heads;
   // Items: prefill items [0, n_pre * H_kv), decode items after them.  Prefill-only and
   // decode-only launches hand them out with one counter.  Mixed launches keep a counter per kind;
@@ -991,7 +1028,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
     } else {
       if constexpr ((kKinds & 2) != 0) {
         const int2 en = a.entries[max_pre + (e - n_pre)];
-        decode_split<D, NW>(a, en.x, en.y, g, vbufA, vbufB);
+        decode_split<D, NW>(a, en.x, en.y, g, pps, vbufA, vbufB);
       }
     }
     __syncthreads();

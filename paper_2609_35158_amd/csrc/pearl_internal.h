@@ -20,7 +20,10 @@ constexpr int kWaves = kThreads / 64;
 constexpr int kRowsPerTile = 256;    // q-rows (token x head-in-group) per prefill work item
 constexpr int kKeysPerStage = 64;    // keys staged in LDS per prefill step (4 pages)
 constexpr int kMinPagesPerSplit = 16;
-constexpr int kMaxPagesPerSplit = 512;   // page ids of one split are staged in LDS
+constexpr int kMaxPagesPerSplit = 512;
+// The planner sizes decode splits from the launch's actual pages: about this many decode items
+// per compute unit (never fewer pages per split than the host's bound, which sizes the workspace).
+constexpr int kDecItemsPerCU = 4;
 // Compute units assumed when sizing decode splits (MI355X has 256).  A fixed value keeps the
 // workspace size a pure function of the shapes; the launch grid uses the device's real count.
 constexpr int kPlanComputeUnits = 256;
@@ -49,6 +52,7 @@ enum Hdr : int {
   kHdrNumPreJobs = 6,  // prefill tiles with more than one split (merge jobs)
   kHdrCounterPre = 7,  // prefill work counter of mixed launches (atomic)
   kHdrPreFirstWG = 8,  // mixed launches: workgroups [0, this) take prefill items first
+  kHdrPagesPerSplit = 9,  // pages per decode split chosen by the planner
   kHdrZero = 32,       // words 32..63: a zeroed 128-byte block (source for keys past the end)
   kHdrWords = 64
 };
@@ -79,7 +83,7 @@ struct PlanParams {
   int num_kv_heads;
   int group;             // G
   int tokens_per_tile;   // kRowsPerTile / G
-  int pages_per_split;
+  int pages_per_split;   // the least pages per decode split (the workspace holds that many splits)
   int64_t max_pre;       // capacity of the prefill entry list
   int64_t max_dec;       // capacity of the decode entry list (and of the partial buffers)
   int64_t pre_slots;     // partial slots for split prefill items
@@ -109,7 +113,6 @@ struct AttnArgs {
   int num_kv_heads;
   int group;
   int tokens_per_tile;
-  int pages_per_split;
   float scale_log2;          // softmax_scale * log2(e)
 };
 
