@@ -752,10 +752,19 @@ def cpu_baseline(torch, case, out, budget_s, pool):
     }
 
 
+def _record_current(e):
+    """True when the sources a profile record was taken from (their files' bytes, concatenated in
+    the recorded order) still hash to the recorded sha256."""
+    import hashlib
+    h = hashlib.sha256()
+    for f in e.get("sources", []):
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return bool(e.get("sources")) and h.hexdigest() == e.get("sources_sha256")
+
+
 def measured_traffic(kernel, workload):
     """HBM bytes per launch recorded from the rocprofv3 counter passes, or None when no record
     exists or the kernel source changed since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
     try:
         data = json.load(open(path))
@@ -763,8 +772,7 @@ def measured_traffic(kernel, workload):
         return None
     for e in data.get("entries", []):
         if e.get("kernel") == kernel and e.get("workload") == workload:
-            src = open(os.path.join(ROOT, e["source"]), "rb").read()
-            if hashlib.sha256(src).hexdigest() != e.get("source_sha256"):
+            if not _record_current(e):
                 return None
             return int(e["read_bytes"]) + int(e["write_bytes"])
     return None
@@ -773,7 +781,6 @@ def measured_traffic(kernel, workload):
 def kernel_counters(kernel, workload):
     """Clock, MFMA use and occupancy of a kernel from the committed rocprofv3 counter pass, or None
     when no record exists or the kernel source changed since the counters were taken."""
-    import hashlib
     path = os.path.join(ROOT, "profiles", "kernel_counters.json")
     try:
         data = json.load(open(path))
@@ -781,8 +788,7 @@ def kernel_counters(kernel, workload):
         return None
     for e in data.get("entries", []):
         if e.get("kernel") == kernel and e.get("workload") == workload:
-            src = open(os.path.join(ROOT, e["source"]), "rb").read()
-            if hashlib.sha256(src).hexdigest() != e.get("source_sha256"):
+            if not _record_current(e):
                 return None
             return {"sclk_mhz": e["sclk_mhz"], "mfma_busy": e["mfma_busy"], "waves_per_cu": e["waves_per_cu"],
                     "mfma_bf16_flop": e["mfma_bf16_flop"], "from": "profiles/kernel_counters.json"}

@@ -45,10 +45,14 @@ def test_launch_stats():
 def test_counter_records_are_tied_to_the_kernel_source():
     data = json.load(open(os.path.join(ROOT, "profiles", "kernel_counters.json")))
     for e in data["entries"]:
-        assert os.path.exists(os.path.join(ROOT, e["source"]))
+        assert e["sources"] and all(os.path.exists(os.path.join(ROOT, f)) for f in e["sources"])
         assert 0 < e["sclk_mhz"] < 3000 and 0 <= e["mfma_busy"] <= 1
-    got = bench.kernel_counters("attn_kernel<128>", "no-such-workload")
-    assert got is None
+    assert bench.kernel_counters("attn_kernel<128>", "no-such-workload") is None
+    # a record whose sources no longer hash to its sha256 is not used
+    e = dict(data["entries"][0])
+    assert bench._record_current(e)
+    e["sources_sha256"] = "0" * 64
+    assert not bench._record_current(e)
 
 
 def test_oracle_pool_baseline_and_parity():
