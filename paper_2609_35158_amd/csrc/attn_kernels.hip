@@ -164,7 +164,8 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
   __syncthreads();
   // pass 1: validate every sequence and total the work
-  int my_pages = 0;                            // decode pages of sequence tid (first chunk)
+  // sequence tid's lengths (first chunk), kept for the later passes
+  int my_pages = 0, my_q_start = 0, my_q_len = 0, my_ctx = 0;
   {
     int tiles = 0, max_full = 0;
     unsigned long long pre_keys = 0, dec_keys = 0, dec_pages = 0;
@@ -172,6 +173,11 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
       const int q_start = cu ? cu[b] : b;
       const int q_len = cu ? cu[b + 1] - q_start : 1;
       const int ctx = ctx_lens[b];
+      if (b == tid) {
+        my_q_start = q_start;
+        my_q_len = q_len;
+        my_ctx = ctx;
+      }
       const long long kv = (long long)ctx + q_len;
       bool bad = q_len < 0 || ctx < 0 || q_start < 0 || q_len > p.max_q_len ||
                  (long long)q_start + q_len > p.total_q || kv > p.max_kv_len ||
@@ -282,9 +288,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     int cnt[4] = {0, 0, 0, 0};              // prefill entries, decode splits, split tiles, full decode splits
     int kind = kSeqNone, q_start = 0, q_len = 0, ctx = 0, nt = 0, rest = 0;
     if (b < p.batch) {
-      q_start = cu ? cu[b] : b;
-      q_len = cu ? cu[b + 1] - q_start : 1;
-      ctx = ctx_lens[b];
+      q_start = base == 0 ? my_q_start : (cu ? cu[b] : b);
+      q_len = base == 0 ? my_q_len : (cu ? cu[b + 1] - q_start : 1);
+      ctx = base == 0 ? my_ctx : ctx_lens[b];
       if (q_len > 0) {
         const bool dec = p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1);
         if (dec) {
@@ -1048,12 +1054,14 @@ __global__ __launch_bounds__(256) void merge_kernel(AttnArgs a, int batch) {
   const int wid = blockIdx.x * 4 + (threadIdx.x >> 6);
   const int H_q = a.num_q_heads;
   if (wid >= batch * H_q) return;
-  if (a.ws_hdr[kHdrError] != 0) return;
   const int b = wid / H_q, h = wid - (wid / H_q) * H_q;
+  // three independent reads (the record and base of a sequence the planner skipped are read but
+  // not used)
+  const int err = a.ws_hdr[kHdrError];
   const SeqInfo si = a.seqinfo[b];
-  const int ns = si.kind >> 4;
-  if ((si.kind & 15) != kSeqDecode || ns <= 1) return;
   const size_t base = (size_t)a.split_base[b];
+  const int ns = si.kind >> 4;
+  if (err != 0 || (si.kind & 15) != kSeqDecode || ns <= 1) return;
   float M = -INFINITY;
   for (int s = lane; s < ns; s += 64) M = fmaxf(M, a.part_ml[2 * ((base + s) * H_q + h)]);
 #pragma unroll
