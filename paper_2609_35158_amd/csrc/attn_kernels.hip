@@ -124,11 +124,14 @@ template <int D, int NW, int kKinds> struct Lds {
 // some rows of the tile see (key ctx + t0 + 1), so every row sees at least one key of every
 // split.  S is at least kMinSplitKeys and at least the tile keys per unit, which keeps the split
 // items of a launch under 2 * kPlanComputeUnits (the partial-slot capacity).
+//
+// Decode splits hold pps pages each (the last one of a sequence the rest): pps is sized from the
+// launch's actual pages (about kDecItemsPerCU items per compute unit) but never below the host's
+// bound, so the workspace always holds the splits.  They are ordered longest first: every full
+// split, then the shorter last splits in kPartBuckets size classes, largest class first, so the
+// last items a launch hands out are its shortest ones.
 // ------------------------------------------------------------------------------------------------
 constexpr int kPlanThreads = 256;
-// Decode splits are ordered longest first: every full split (pages_per_split pages), then each
-// sequence's shorter last split in kPartBuckets size classes, largest class first, so the last
-// items a launch hands out are its shortest ones.
 constexpr int kPartBuckets = 16;
 
 // Size class of a short last split of `rest` pages (1 <= rest < pps); class 0 holds the longest.
@@ -702,9 +705,9 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
 }
 
 // ------------------------------------------------------------------------------------------------
-// Decode work item: one (sequence, kv-head g, split of pages_per_split pages).  The G q-heads of
-// the group are the 16 columns of 16x16x32 MFMAs (columns >= G are zero), so each K/V byte is
-// loaded once for the whole group.  Wave w takes page pairs w, w+8, ... of the split:
+// Decode work item: one (sequence, kv-head g, split of pps pages; the planner chooses pps).  The
+// G q-heads of the group are the 16 columns of 16x16x32 MFMAs (columns >= G are zero), so each
+// K/V byte is loaded once for the whole group.  Wave w takes page pairs w, w+8, ... of the split:
 //   S^T (16 keys x heads) = K_page . Q^T          (A = K straight from HBM into registers)
 //   O^T (dims x heads)   += V^T . P^T over 32 keys (A = V^T read transposed from LDS)
 // V travels HBM -> LDS with 16-byte LDS-DMA loads (no VGPRs, no LDS store instructions) into a
