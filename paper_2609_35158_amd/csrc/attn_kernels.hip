@@ -284,8 +284,9 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   if (tid < kPartBuckets) s_part_cnt[tid] = 0;   // now the fill count of each class
   __syncthreads();
   const int S = s_split_keys;
-  // pass 2: per-sequence counts (prefill entries, decode entries, split tiles), block-wide
-  // exclusive scans, then the entries: prefill tiles last (longest) tile first, splits in order
+  // pass 2: per-sequence counts (prefill entries, decode splits, split tiles, full decode splits),
+  // block-wide exclusive scans, then the entries: prefill tiles last (longest) tile first with
+  // their key splits in order; decode splits longest first (full splits, then size classes)
   for (int base = 0; base < p.batch; base += kPlanThreads) {
     const int b = base + tid;
     int cnt[4] = {0, 0, 0, 0};              // prefill entries, decode splits, split tiles, full decode splits
