@@ -243,11 +243,17 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     s_pre_first = pre_first;
     // Decode split size: about kDecItemsPerCU items per compute unit over the launch's actual
     // pages, a multiple of 16 pages, at least the host's bound and at most kMaxPagesPerSplit.
+    // Splits of at least kDecLongSplitPages pages (8 page pairs per wave) while that still leaves
+    // 2 items per compute unit: a wave's first pair of an item waits unhidden, so short splits
+    // pay it often.
     long long pps = p.pages_per_split;
     if (s_dec_pages > 0) {
+      const long long units = (long long)s_dec_pages * H;
       const long long per = (long long)kPlanComputeUnits * kDecItemsPerCU;
-      const long long want = ((long long)s_dec_pages * H + per - 1) / per;
+      const long long want = (units + per - 1) / per;
+      const long long two = (units + 2LL * kPlanComputeUnits - 1) / (2LL * kPlanComputeUnits);
       pps = max(pps, (want + 15) / 16 * 16);
+      pps = max(pps, min((long long)kDecLongSplitPages, (two + 15) / 16 * 16));
       pps = min(pps, (long long)max(p.pages_per_split, kMaxPagesPerSplit));
     }
     s_pps = (int)pps;

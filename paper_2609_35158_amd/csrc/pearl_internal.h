@@ -24,6 +24,7 @@ constexpr int kMaxPagesPerSplit = 512;
 // The planner sizes decode splits from the launch's actual pages: about this many decode items
 // per compute unit (never fewer pages per split than the host's bound, which sizes the workspace).
 constexpr int kDecItemsPerCU = 4;
+constexpr int kDecLongSplitPages = 128;
 // Compute units assumed when sizing decode splits (MI355X has 256).  A fixed value keeps the
 // workspace size a pure function of the shapes; the launch grid uses the device's real count.
 constexpr int kPlanComputeUnits = 256;
