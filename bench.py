@@ -318,7 +318,9 @@ def hbm_probe(torch, nbytes=1 << 30, reps=10):
     t_copy = timed(lambda: bd.hbm_copy(src, dst))
     gbps = lambda moved, t: round(moved / (t * 1e-3) / 1e9, 1)
     fig = {"bytes": nbytes, "what": "library streaming kernels (pearl_hbm_read / _fill / _copy), 16-byte "
-                                    "vectors, median of %d launches each after a 1 GiB read flush" % reps,
+                                    "vectors, median of %d launches each after a 1 GiB read flush; the "
+                                    "write and copy figures exclude write-back still pending in the "
+                                    "caches when the kernel ends" % reps,
            "read_GBps": gbps(nbytes, t_read[0]), "write_GBps": gbps(nbytes, t_write[0]),
            "copy_GBps": gbps(2 * nbytes, t_copy[0]),
            "read_GBps_best": gbps(nbytes, t_read[1]), "copy_GBps_best": gbps(2 * nbytes, t_copy[1])}
