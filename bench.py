@@ -812,7 +812,7 @@ def cpu_model():
 def main():
     args = parse()
     if args.gpus != 1:
-        print("bench.py measures one GPU only: this build has no multi-GPU path (attention shards by "
+        print("bench.py measures one GPU only: the library has no multi-GPU path (attention shards by "
               "sequence and kv-head with no exchange; see the sharding notes). Run with --gpus 1.",
               file=sys.stderr)
         sys.exit(2)
