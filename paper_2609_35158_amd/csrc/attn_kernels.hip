@@ -448,8 +448,10 @@ template <int D> struct DmaTile {
 // A split item (entry e, code = tile | split << 16) covers only its key range and writes the
 // unnormalised (o~, m, l) of its rows to partial slot e * H_kv + g for the prefill merge.
 // ------------------------------------------------------------------------------------------------
-// kHoistV: read the first dim block's V^T operands before the softmax (needs 16 more VGPRs; used
-// where the kernel has them to spare).
+// kHoistV (prefill-only kernels, which have registers and instruction cache to spare): read the
+// first dim block's V^T operands before the softmax (16 more VGPRs) and unroll the stage loop over
+// the three buffers.  The mixed kernel, short of both, selects the buffers at run time instead,
+// which keeps its code small (measured faster there; the unrolled form is faster alone).
 // Stages travel by LDS-DMA into three DmaTile buffers per tensor (kb*, vb*), two stages ahead.
 template <int D, bool kHoistV>
 __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
@@ -458,8 +460,10 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
   using DT = DmaTile<D>;
   constexpr int RB = DT::RB;
-  auto kbuf = [&](int buf) { return buf == 0 ? kb0 : (buf == 1 ? kb1 : kb2); };
-  auto vbuf = [&](int buf) { return buf == 0 ? vb0 : (buf == 1 ? vb1 : vb2); };
+  // the unrolled loop names each buffer by a constant; the run-time loop needs contiguous
+  // buffers (k/vb1 = k/vb0 + BYTES, k/vb2 = k/vb0 + 2 * BYTES), which its caller provides
+  auto kbuf = [&](int buf) { return kHoistV ? (buf == 0 ? kb0 : (buf == 1 ? kb1 : kb2)) : kb0 + buf * DT::BYTES; };
+  auto vbuf = [&](int buf) { return kHoistV ? (buf == 0 ? vb0 : (buf == 1 ? vb1 : vb2)) : vb0 + buf * DT::BYTES; };
 
   const int lane = threadIdx.x & 63, half = lane >> 5;
   const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
@@ -664,18 +668,26 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   dma_stage(step_begin, 0);
   if (step_begin + 1 < step_end) dma_stage(step_begin + 1, 1);
   close_stage(false);
-  for (int step = step_begin; step < step_end; step += 3) {
-    if (step + 2 < step_end) dma_stage(step + 2, 2);
-    compute(step, 0);
-    close_stage(step + 2 < step_end);
-    if (step + 1 >= step_end) break;
-    if (step + 3 < step_end) dma_stage(step + 3, 0);
-    compute(step + 1, 1);
-    close_stage(step + 3 < step_end);
-    if (step + 2 >= step_end) break;
-    if (step + 4 < step_end) dma_stage(step + 4, 1);
-    compute(step + 2, 2);
-    close_stage(step + 4 < step_end);
+  if constexpr (kHoistV) {
+    for (int step = step_begin; step < step_end; step += 3) {
+      if (step + 2 < step_end) dma_stage(step + 2, 2);
+      compute(step, 0);
+      close_stage(step + 2 < step_end);
+      if (step + 1 >= step_end) break;
+      if (step + 3 < step_end) dma_stage(step + 3, 0);
+      compute(step + 1, 1);
+      close_stage(step + 3 < step_end);
+      if (step + 2 >= step_end) break;
+      if (step + 4 < step_end) dma_stage(step + 4, 1);
+      compute(step + 2, 2);
+      close_stage(step + 4 < step_end);
+    }
+  } else {
+    for (int step = step_begin, buf = 0; step < step_end; ++step, buf = buf == 2 ? 0 : buf + 1) {
+      if (step + 2 < step_end) dma_stage(step + 2, buf == 0 ? 2 : buf - 1);
+      compute(step, buf);
+      close_stage(step + 2 < step_end);
+    }
   }
 
   // epilogue: combine the two half-row sums; a split item stores its fp32 partial state
@@ -1040,7 +1052,8 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
           static_assert(6 * B <= Lds<D, NW, kKinds>::bytes, "stage buffers fit the shared region");
           prefill_tile<D, false>(a, e, en.x, en.y, g, split_keys, smem, smem + B, smem + 2 * B,
                                        smem + 3 * B, smem + 4 * B, smem + 5 * B);
-        }      }
+        }
+      }
     } else {
       if constexpr ((kKinds & 2) != 0) {
         const int2 en = a.entries[max_pre + (e - n_pre)];
