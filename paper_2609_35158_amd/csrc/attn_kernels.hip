@@ -140,6 +140,12 @@ __device__ __forceinline__ int part_bucket(int rest, float inv_pps) {
   return kPartBuckets - 1 - min(kPartBuckets - 1, (int)((float)(rest - 1) * inv_pps));
 }
 
+// Size class of an unsplit prefill tile whose first row sees `keys` keys (at most max_full;
+// inv_keys = kPartBuckets / (max_full + 1)): the longest tiles are class 0.
+__device__ __forceinline__ int tile_class(int keys, float inv_keys) {
+  return kPartBuckets - 1 - min(kPartBuckets - 1, (int)((float)keys * inv_keys));
+}
+
 __device__ __forceinline__ int tile_splits(int ctx, int t0, int split_keys) {
   return split_keys > 0 ? (ctx + t0 + split_keys) / split_keys : 1;   // ceil((ctx + t0 + 1) / S)
 }
@@ -157,13 +163,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __shared__ unsigned long long s_dec_pages;
   __shared__ int s_part_cnt[kPartBuckets];     // short last splits per size class, then fill counts
   __shared__ int s_part_off[kPartBuckets];     // first position of each size class after the full splits
+  __shared__ int s_tile_cnt[kPartBuckets];     // unsplit prefill tiles per size class, then fill counts
+  __shared__ int s_tile_off[kPartBuckets];     // first prefill entry of each size class
   const int tid = threadIdx.x;
   const int T = p.tokens_per_tile;
   if (tid == 0) {
     s_err = 0; s_tiles = 0; s_max_full = 0; s_pre_keys = 0; s_dec_keys = 0; s_n_full = 0; s_dec_pages = 0;
     s_carry[0] = s_carry[1] = s_carry[2] = s_carry[3] = 0;
   }
-  if (tid < kPartBuckets) s_part_cnt[tid] = 0;
+  if (tid < kPartBuckets) { s_part_cnt[tid] = 0; s_tile_cnt[tid] = 0; }
   if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
   __syncthreads();
   // pass 1: validate every sequence and total the work
@@ -261,38 +269,47 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __syncthreads();
   const int pps = s_pps;
   const float inv_pps = (float)kPartBuckets / (float)pps;
-  // pass 1b: full decode splits and the size classes of the short last splits
+  const int S = s_split_keys;
+  const float inv_keys = (float)kPartBuckets / (float)(s_max_full + 1);
+  // pass 1b: full decode splits and the size classes of the short last splits; without key
+  // splits, the size classes of the prefill tiles too
   {
     int n_full = 0;
     for (int b = tid; b < p.batch; b += kPlanThreads) {
-      int pages = my_pages;
+      int pages = my_pages, q_len = my_q_len, ctx = my_ctx;
+      bool dec = pages > 0;
       if (b != tid) {
         const int q_start = cu ? cu[b] : b;
-        const int q_len = cu ? cu[b + 1] - q_start : 1;
-        const bool dec = p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1);
-        pages = dec ? (ctx_lens[b] + q_len + kPage - 1) / kPage : 0;
+        q_len = cu ? cu[b + 1] - q_start : 1;
+        ctx = ctx_lens[b];
+        dec = p.mode == kModeDecode || (p.mode == kModeMixed && q_len == 1);
+        pages = dec ? (ctx + q_len + kPage - 1) / kPage : 0;
       }
       if (pages > 0) {
         const int rest = pages % pps;
         n_full += pages / pps;
         if (rest) atomicAdd(&s_part_cnt[part_bucket(rest, inv_pps)], 1);
+      } else if (!dec && q_len > 0 && S == 0) {
+        const int nt = (q_len + T - 1) / T;
+        for (int t = 0; t < nt; ++t) atomicAdd(&s_tile_cnt[tile_class(ctx + t * T + 1, inv_keys)], 1);
       }
     }
     if (n_full) atomicAdd(&s_n_full, n_full);
   }
   __syncthreads();
-  if (tid < kPartBuckets) {                   // size classes, largest first, after the full splits
-    int off = s_n_full;
-    for (int k = 0; k < tid; ++k) off += s_part_cnt[k];
+  if (tid < kPartBuckets) {                   // size classes, largest first (decode: after the full splits)
+    int off = s_n_full, toff = 0;
+    for (int k = 0; k < tid; ++k) { off += s_part_cnt[k]; toff += s_tile_cnt[k]; }
     s_part_off[tid] = off;
+    s_tile_off[tid] = toff;
   }
   __syncthreads();
-  if (tid < kPartBuckets) s_part_cnt[tid] = 0;   // now the fill count of each class
+  if (tid < kPartBuckets) { s_part_cnt[tid] = 0; s_tile_cnt[tid] = 0; }   // now the fill counts
   __syncthreads();
-  const int S = s_split_keys;
   // pass 2: per-sequence counts (prefill entries, decode splits, split tiles, full decode splits),
-  // block-wide exclusive scans, then the entries: prefill tiles last (longest) tile first with
-  // their key splits in order; decode splits longest first (full splits, then size classes)
+  // block-wide exclusive scans, then the entries: prefill tiles longest first (unsplit tiles by
+  // size class across the launch; key-split tiles per sequence, last tile first, splits in
+  // order); decode splits longest first (full splits, then size classes)
   for (int base = 0; base < p.batch; base += kPlanThreads) {
     const int b = base + tid;
     int cnt[4] = {0, 0, 0, 0};              // prefill entries, decode splits, split tiles, full decode splits
@@ -346,12 +363,29 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     if (b < p.batch) {
       seqinfo[b] = SeqInfo{q_start, q_len, ctx, kind | (cnt[1] << 4)};
       split_base[b] = excl[1];
-      int e = excl[0], j = excl[2];
-      for (int t = nt - 1; t >= 0; --t) {
-        const int ns = tile_splits(ctx, t * T, S);
-        if (ns > 1 && j < p.pre_jobs_cap) pre_jobs[j++] = make_int4(b, t, e, ns);
-        for (int sp = 0; sp < ns; ++sp, ++e)
-          if (e < p.max_pre) entries[e] = make_int2(b, t | (sp << 16));
+      if (S == 0) {
+        // unsplit tiles go longest first across the whole launch (by size class), so the last
+        // tiles the persistent grid hands out are short ones from any sequence.  A sequence's
+        // tiles of one class (a run of consecutive tiles) are claimed together and stay
+        // adjacent, so the tiles that read the same K/V still run at about the same time.
+        for (int t = nt - 1; t >= 0;) {
+          const int k = tile_class(ctx + t * T + 1, inv_keys);
+          int t_end = t;
+          while (t_end > 0 && tile_class(ctx + (t_end - 1) * T + 1, inv_keys) == k) --t_end;
+          int pos = s_tile_off[k] + atomicAdd(&s_tile_cnt[k], t - t_end + 1);
+          for (; t >= t_end; --t, ++pos)
+            if (pos < p.max_pre) entries[pos] = make_int2(b, t);
+        }
+      } else {
+        // key-split tiles: each tile's splits stay contiguous (their partial slots follow the
+        // entry index), last tile of the sequence first
+        int e = excl[0], j = excl[2];
+        for (int t = nt - 1; t >= 0; --t) {
+          const int ns = tile_splits(ctx, t * T, S);
+          if (ns > 1 && j < p.pre_jobs_cap) pre_jobs[j++] = make_int4(b, t, e, ns);
+          for (int sp = 0; sp < ns; ++sp, ++e)
+            if (e < p.max_pre) entries[e] = make_int2(b, t | (sp << 16));
+        }
       }
       // full splits in sequence order; the short last split at its size class's next position
       // (claimed before the loop, so the wave issues the atomic once)
