@@ -413,3 +413,38 @@ def test_batches_larger_than_one_planner_chunk():
         torch.cuda.synchronize()
         m = np.isfinite(o_ref).all(axis=(1, 2))
         assert_close(bits(out)[m], o_ref[m], lse.cpu().numpy()[m], l_ref[m], what="1100-sequence " + mode)
+
+
+def test_prefill_tile_order_spans_chunks():
+    """Prefill of 300 sequences with up to 4 tiles each and no key splits: tiles are written by
+    size class across the whole launch, a sequence's run of tiles in one class claimed together,
+    and the classes and runs span the planner's 256-sequence chunks.  Every row's LSE (preset to
+    NaN) must be written, and sampled sequences match the oracle."""
+    from gpu_helpers import oracle_sampled
+    from paper_2609_35158_amd import binding as bd
+    say("case: 300-sequence prefill, tiles ordered by size class")
+    rng = np.random.default_rng(79)
+    ctx = rng.integers(0, 2000, size=300, endpoint=True)
+    ql = rng.integers(1, 256, size=300, endpoint=True)
+    ctx[:4] = (0, 2000, 0, 1999)
+    ql[:4] = (256, 256, 1, 65)
+    case = workloads.build_case("prefill-order", 7704, 8, 2, 64, ctx, ql, device="cuda")
+    gpu_append(case)
+    dctx, cu = dev_lengths(case)
+    max_q, max_kv = bounds(case)
+    desc = bd.make_desc(case.block_table, dctx, cu, case.total_q, max_q, max_kv)
+    ws = torch.empty(bd.workspace_bytes(case.num_q_heads, case.k_pool, desc), dtype=torch.uint8, device="cuda")
+    lse = torch.full((case.total_q, case.num_q_heads), float("nan"), dtype=torch.float32, device="cuda")
+    out, lse = pa.prefill_append(case.q, case.k_pool, case.v_pool, case.block_table, dctx, cu, max_q, max_kv,
+                                 scale=case.scale, return_lse=True, lse=lse, workspace=ws)
+    torch.cuda.synchronize()
+    hdr = ws[:64 * 4].view(torch.int32).cpu().numpy()
+    assert hdr[5] == 0, "expected no key splits"
+    lse_np = lse.cpu().numpy()
+    assert np.isfinite(lse_np).all(), "rows left unwritten: %d" % int((~np.isfinite(lse_np)).sum())
+    seqs = [0, 1, 2, 3] + sorted(int(x) for x in rng.choice(np.arange(4, 300), 20, replace=False))
+    o_ref, l_ref = oracle_sampled(case, seqs)
+    o = bits(out)
+    for b in seqs:
+        r = slice(int(case.cu_q_lens[b]), int(case.cu_q_lens[b] + case.q_lens[b]))
+        assert_close(o[r], o_ref[b], lse_np[r], l_ref[b], what="prefill-order sequence %d" % b)
