@@ -16,6 +16,8 @@ from paper_2609_35158_amd import workloads
 MAX_ABS = 1e-2
 MEAN_ABS = 1e-3
 LSE_ABS = 1e-3
+# Stress cases only: from this |o| on, the bar adds bf16 ulps of the reference (assert_close).
+SLACK_FROM = 4.0
 
 
 def say(*a):
@@ -111,8 +113,11 @@ def bf16_ulp(x: np.ndarray) -> np.ndarray:
 def assert_close(gpu_o_bits: np.ndarray, ref_o: np.ndarray, gpu_lse: Optional[np.ndarray] = None,
                  ref_lse: Optional[np.ndarray] = None, what: str = "", ulp_slack: float = 0.0) -> dict:
     """Outputs within max-abs 1e-2 and mean-abs 1e-3 of the float64 oracle.  With ulp_slack > 0
-    (stress inputs whose outputs reach |o| >= 4, where rounding to bf16 alone moves a value by up
-    to 2^-9 |o| > 1e-2), each element may also deviate by ulp_slack bf16 ulps of the reference."""
+    (stress inputs whose outputs reach |o| >= 4), elements whose reference has |o| >= SLACK_FROM
+    may also deviate by ulp_slack bf16 ulps of the reference: there, rounding the output to bf16
+    alone moves a value by up to half an ulp (2^-6 |o| / 2 >= 0.0156 > 1e-2), and the weights
+    entering P.V as bf16 add up to 2^-9 sum_j w_j |v_j| / l, another half ulp when one key
+    dominates.  Every other element keeps the plain 1e-2 bar."""
     st = oracle.compare(gpu_o_bits, ref_o)
     say("   parity %s: n=%d max_abs=%.3e mean_abs=%.3e max_ulp=%.1f" % (what, st["n"], st["max_abs"],
                                                                           st["mean_abs"], st["max_ulp"]))
@@ -121,8 +126,11 @@ def assert_close(gpu_o_bits: np.ndarray, ref_o: np.ndarray, gpu_lse: Optional[np
     if ulp_slack > 0:
         g = oracle.bf16_bits_to_f64(gpu_o_bits)
         m = np.isfinite(ref_o)
-        excess = np.abs(g[m] - ref_o[m]) - (MAX_ABS + ulp_slack * bf16_ulp(ref_o[m]))
-        assert excess.max() <= 0, "max excess over 1e-2 + %g ulp: %.3e (%s)" % (ulp_slack, excess.max(), what)
+        r = ref_o[m]
+        bar = MAX_ABS + np.where(np.abs(r) >= SLACK_FROM, ulp_slack * bf16_ulp(r), 0.0)
+        excess = np.abs(g[m] - r) - bar
+        assert excess.max() <= 0, "max excess over the bar (1e-2, + %g ulp where |o| >= %g): %.3e (%s)" % (
+            ulp_slack, SLACK_FROM, excess.max(), what)
     else:
         assert st["max_abs"] <= MAX_ABS, "max_abs %.3e > %.1e (%s)" % (st["max_abs"], MAX_ABS, what)
     assert st["mean_abs"] <= MEAN_ABS, "mean_abs %.3e > %.1e (%s)" % (st["mean_abs"], MEAN_ABS, what)
