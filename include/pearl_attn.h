@@ -28,8 +28,9 @@
  *     [head_dim]; lse: fp32 [total_q][num_q_heads].  Rows of sequence b are rows
  *     cu_q_lens[b] .. cu_q_lens[b+1]-1 (row b when cu_q_lens is NULL).
  *   - `stream` is a hipStream_t (NULL = the null stream).  Calls are asynchronous on it; the
- *     library allocates no device memory, keeps no pointer after returning and holds no state
- *     between calls apart from per-device launch parameters queried once.
+ *     library allocates no device memory and keeps no pointer after returning.  The state it holds
+ *     between calls is the per-device launch parameters it queries once, and the calling
+ *     thread's timing-event pair while one is set (pearl_set_kernel_events).
  *   - Supported: head_dim 64 or 128; page_size 16; G = num_q_heads/num_kv_heads in {1,2,4,8};
  *     max_q_len <= 2^21 and max_kv_len <= 2^25.  Anything else returns PEARL_ERR_UNSUPPORTED.
  *   - Host-checkable errors (NULL pointers, bad shapes, batch <= 0, sizes inconsistent with each
