@@ -140,22 +140,26 @@ def pin_assert_close_bars():
     assert_close(g, np.full(n, 1.0 - 0.0009), what="under the mean bar")
 
 
-def pin_ulp_slack_only_at_large_outputs():
-    """The stress-case slack (1 bf16 ulp of the reference, added to 1e-2) applies only where the
-    reference has |o| >= 4: an error of 0.03 passes at 6.0 (ulp 2^-5), and 0.02 fails at 3.0
-    (ulp 2^-6, so 0.02 would pass if the slack applied there)."""
-    n = 200
-    g = np.array([bf16(0, 2, 64)] + [bf16(0, 0, 0)] * (n - 1), np.uint16)   # 6.0, then ones
+def pin_peaked_bound():
+    """The stress-case bar: max(1e-2, half an ulp of the reference + 2^-8 vmax + 1e-4).  With
+    vmax = 5: at 3.0 (ulp 2^-6) the bar is 2^-7 + 5/256 + 1e-4 = 0.027444, so 0.0274 passes and
+    0.0275 fails; at 6.0 (ulp 2^-5) it is 2^-6 + 5/256 + 1e-4 = 0.035256, so 0.0352 passes and
+    0.0353 fails.  With vmax = 2 at 2^-5 the bound (0.00797) is below 1e-2, so the plain bar
+    holds: 0.0099 passes and 0.0101 fails."""
+    n = 400
+    ones = [bf16(0, 0, 0)] * (n - 1)
+    for top, vmax, err_ok, err_bad in (((0, 1, 64), 5.0, 0.0274, 0.0275), ((0, 2, 64), 5.0, 0.0352, 0.0353),
+                                       ((0, -5, 0), 2.0, 0.0099, 0.0101)):
+        g = np.array([bf16(*top)] + ones, np.uint16)
+        ref = np.ones(n)
+        ref[0] = bf16_value(*top) - err_ok
+        assert_close(g, ref, what="peaked ok", peaked_vmax=vmax)
+        ref[0] = bf16_value(*top) - err_bad
+        assert _raises(lambda: assert_close(g, ref, what="peaked bad", peaked_vmax=vmax))
+    g = np.array([bf16(0, 1, 64)] + ones, np.uint16)
     ref = np.ones(n)
-    ref[0] = 6.0 - 0.03
-    assert_close(g, ref, what="slack at 6", ulp_slack=1.0)
-    assert _raises(lambda: assert_close(g, ref, what="no slack", ulp_slack=0.0))
-    ref[0] = 6.0 - 0.045                                               # beyond 1e-2 + 1 ulp
-    assert _raises(lambda: assert_close(g, ref, what="past the slack", ulp_slack=1.0))
-    g2 = np.array([bf16(0, 1, 64)] + [bf16(0, 0, 0)] * (n - 1), np.uint16)  # 3.0, then ones
-    ref2 = np.ones(n)
-    ref2[0] = 3.0 - 0.02                                               # over 1e-2, under 1e-2 + 1 ulp
-    assert _raises(lambda: assert_close(g2, ref2, what="no slack below 4", ulp_slack=1.0))
+    ref[0] = 3.0 - 0.0274
+    assert _raises(lambda: assert_close(g, ref, what="no peaked bound"))
 
 
 def pin_lse_bar():
@@ -173,6 +177,6 @@ def pin_lse_bar():
 
 ALL_PINS = [pin_known_offsets, pin_max_is_absolute, pin_ulp_units, pin_gpu_nan_counts,
             pin_reference_nan_excluded, pin_empty_selection, pin_rounded_reference_half_ulp,
-            pin_assert_close_bars, pin_ulp_slack_only_at_large_outputs, pin_lse_bar]
+            pin_assert_close_bars, pin_peaked_bound, pin_lse_bar]
 
 assert math.isclose(bf16_value(0, -2, 64), 0.375)

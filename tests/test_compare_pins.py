@@ -92,11 +92,28 @@ def test_compare_mutation_is_caught(name, monkeypatch):
     assert failed, "mutation %s passed every pin" % name
 
 
-def test_assert_close_threshold_mutation_is_caught(monkeypatch):
-    """A bar read from the wrong constant (the mean bar used as the max bar, or the slack applied
-    at every magnitude) must fail a pin too."""
+def _bound_full_ulp(ref_o, vmax):
     import gpu_helpers
-    monkeypatch.setattr(gpu_helpers, "SLACK_FROM", 0.0)
+    return np.maximum(gpu_helpers.MAX_ABS, gpu_helpers.bf16_ulp(ref_o) + vmax * 2.0 ** -8 + 1e-4)
+
+
+def _bound_without_weights(ref_o, vmax):
+    import gpu_helpers
+    return np.maximum(gpu_helpers.MAX_ABS, 0.5 * gpu_helpers.bf16_ulp(ref_o) + 1e-4)
+
+
+def _bound_weights_half(ref_o, vmax):
+    import gpu_helpers
+    return np.maximum(gpu_helpers.MAX_ABS, 0.5 * gpu_helpers.bf16_ulp(ref_o) + vmax * 2.0 ** -9 + 1e-4)
+
+
+@pytest.mark.parametrize("fn", [_bound_full_ulp, _bound_without_weights, _bound_weights_half],
+                         ids=lambda f: f.__name__)
+def test_peaked_bound_mutation_is_caught(fn, monkeypatch):
+    """A stress bound with a whole ulp for the output rounding, without the bf16-weight term, or
+    with that term at half its size, must fail a pin."""
+    import gpu_helpers
     import compare_pins
+    monkeypatch.setattr(gpu_helpers, "peaked_bound", fn)
     with pytest.raises(AssertionError):
-        compare_pins.pin_ulp_slack_only_at_large_outputs()
+        compare_pins.pin_peaked_bound()
