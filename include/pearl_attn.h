@@ -170,6 +170,26 @@ pearl_status pearl_attn_mixed(const pearl_kv_shape* shape, const pearl_seq_desc*
                               void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Decode without a caller workspace, for callers that cannot allocate device memory at call
+ * time (code under HIP graph capture, tight serving loops, harnesses that forbid allocation).
+ * Same arguments, kernels and results as pearl_attn_decode, bit for bit; the workspace is instead
+ * a static device array of the library, one per GPU (pearl_attn_decode_static_max_bytes() bytes,
+ * 32 MiB), which each GPU the library runs on holds until the process ends.  The call allocates
+ * nothing: no hipMalloc, no hipFree, no allocating library routine.  The array's device address
+ * is looked up on the first call made on each device.
+ *   - A batch whose workspace (pearl_attn_workspace_bytes) exceeds the limit returns
+ *     PEARL_ERR_UNSUPPORTED before any HIP call; use pearl_attn_decode for it.
+ *   - Every call on one GPU shares that GPU's array and leaves its contents behind; each call
+ *     rebuilds what it reads, so no clearing is needed between calls.  Calls that overlap on one
+ *     GPU (on different streams, or from different threads without ordering) race on the array
+ *     and give undefined results: order them on one stream.
+ */
+size_t pearl_attn_decode_static_max_bytes(void);
+pearl_status pearl_attn_decode_static(const pearl_kv_shape* shape, const pearl_seq_desc* seqs,
+                                      const void* q, const void* k_pool, const void* v_pool,
+                                      float softmax_scale, void* out, float* lse, void* stream);
+
+/*
  * KV transfer between pools (paper, section 4.3, Eq. 3: under PD disaggregation the prefill
  * pool hands each turn's new-token K/V to the decode pool; the transfer takes B * dL * K / BW).
  * pearl_kv_pack gathers, for every sequence b, the K and V rows of positions ctx_lens[b] ..

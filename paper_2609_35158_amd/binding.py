@@ -42,7 +42,8 @@ class SeqDesc(ctypes.Structure):
 EXPORTED = ("pearl_abi_version", "pearl_status_str", "pearl_last_error", "pearl_kv_append",
             "pearl_attn_workspace_bytes", "pearl_attn_prefill_append", "pearl_attn_decode",
             "pearl_attn_mixed", "pearl_kv_pack", "pearl_kv_unpack", "pearl_set_kernel_events",
-            "pearl_hbm_copy", "pearl_hbm_read", "pearl_hbm_fill")
+            "pearl_hbm_copy", "pearl_hbm_read", "pearl_hbm_fill", "pearl_attn_decode_static",
+            "pearl_attn_decode_static_max_bytes")
 
 
 def load(path: str = LIB_PATH):
@@ -77,6 +78,12 @@ def load(path: str = LIB_PATH):
         f.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                       ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                       ctypes.c_size_t, ctypes.c_void_p]
+    lib.pearl_attn_decode_static.restype = ctypes.c_int
+    lib.pearl_attn_decode_static.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p]
+    lib.pearl_attn_decode_static_max_bytes.restype = ctypes.c_size_t
+    lib.pearl_attn_decode_static_max_bytes.argtypes = []
     lib.pearl_set_kernel_events.restype = None
     lib.pearl_set_kernel_events.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
     # measurement tooling (include/pearl_bench.h)
@@ -264,6 +271,37 @@ def decode(q, k_pool, v_pool, block_table, ctx_lens, max_kv_len, scale=None, ret
     """Single-token decode for every sequence (pearl_attn_decode); q is [batch][H_q][d]."""
     return _attention("pearl_attn_decode", q, k_pool, v_pool, block_table, ctx_lens, None,
                       1, max_kv_len, scale, return_lse, out, lse, workspace)
+
+
+def decode_static(q, k_pool, v_pool, block_table, ctx_lens, max_kv_len, scale=None, return_lse=False,
+                  out=None, lse=None):
+    """Single-token decode with the library's static per-GPU workspace (pearl_attn_decode_static):
+    no device memory is allocated by the call (out and lse are allocated here only when not
+    given)."""
+    for t, n in ((q, "q"), (k_pool, "k_pool"), (v_pool, "v_pool")):
+        _need(t, n, torch.bfloat16)
+    if q.dim() != 3:
+        raise ValueError("q must be [batch][num_q_heads][head_dim]")
+    batch, H_q, d = q.shape
+    desc = make_desc(block_table, ctx_lens, None, batch, 1, max_kv_len)
+    shape = make_shape(H_q, k_pool)
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", torch.bfloat16)
+    if return_lse and lse is None:
+        lse = torch.empty((batch, H_q), dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse, "lse", torch.float32)
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    st = load().pearl_attn_decode_static(ctypes.byref(shape), ctypes.byref(desc), q.data_ptr(), k_pool.data_ptr(),
+                                         v_pool.data_ptr(), float(scale), out.data_ptr(), _ptr(lse), _stream())
+    _check(st, "pearl_attn_decode_static")
+    return (out, lse) if (return_lse or lse is not None) else out
+
+
+def decode_static_max_bytes() -> int:
+    return int(load().pearl_attn_decode_static_max_bytes())
 
 
 def mixed(q, k_pool, v_pool, block_table, ctx_lens, cu_q_lens, max_q_len, max_kv_len, scale=None,

@@ -123,9 +123,11 @@ Plan make_plan(const pearl_kv_shape* s, const pearl_seq_desc* q, int mode) {
   return pl;
 }
 
+// static_ws: use the library's static per-device workspace (pearl_attn_decode_static) instead of
+// the caller's ws / ws_bytes; its address is looked up only after every host check has passed.
 pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_desc* q, const void* qp,
                            const void* k_pool, const void* v_pool, float scale, void* out, float* lse,
-                           void* ws, size_t ws_bytes, void* stream) {
+                           void* ws, size_t ws_bytes, void* stream, bool static_ws = false) {
   g_err[0] = 0;
   pearl_status st = check_shape(s);
   if (st != PEARL_OK) return st;
@@ -134,10 +136,11 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   if (mode == kModeDecode && q->cu_q_lens)
     return fail(PEARL_ERR_INVALID_ARG, "pearl_attn_decode requires cu_q_lens == NULL (one token per sequence)");
   if (!qp || !k_pool || !v_pool || !out) return fail(PEARL_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be non-NULL");
-  if (!ws) return fail(PEARL_ERR_WORKSPACE, "workspace is NULL");
+  if (!ws && !static_ws) return fail(PEARL_ERR_WORKSPACE, "workspace is NULL");
   if (!aligned16(qp) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
     return fail(PEARL_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
-  if ((reinterpret_cast<uintptr_t>(ws) & 255) != 0) return fail(PEARL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
+  if (!static_ws && (reinterpret_cast<uintptr_t>(ws) & 255) != 0)
+    return fail(PEARL_ERR_WORKSPACE, "workspace must be 256-byte aligned");
   if (lse && (reinterpret_cast<uintptr_t>(lse) & 3) != 0) return fail(PEARL_ERR_INVALID_ARG, "lse must be 4-byte aligned");
   if (!(scale > 0.f) || !std::isfinite(scale)) return fail(PEARL_ERR_INVALID_ARG, "softmax_scale must be finite and > 0");
   const int64_t total_rows = (int64_t)q->total_q * s->num_q_heads * s->head_dim;
@@ -147,6 +150,15 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   if ((pl.lay.max_pre + pl.lay.max_dec) * (int64_t)s->num_kv_heads > INT32_MAX)
     return fail(PEARL_ERR_UNSUPPORTED, "work list bound (%lld entries x %d kv-heads) exceeds int32",
                 (long long)(pl.lay.max_pre + pl.lay.max_dec), s->num_kv_heads);
+  if (static_ws) {
+    if (pl.lay.total > kStaticScratchBytes)
+      return fail(PEARL_ERR_UNSUPPORTED, "this batch needs %zu bytes of workspace, above the static limit of %zu "
+                  "bytes (use pearl_attn_decode with a caller workspace)", pl.lay.total, kStaticScratchBytes);
+    hipError_t se = hipSuccess;
+    ws = static_scratch(&se);
+    if (!ws) return fail(PEARL_ERR_HIP, "static workspace address: %s", hipGetErrorString(se));
+    ws_bytes = kStaticScratchBytes;
+  }
   if (ws_bytes < pl.lay.total)
     return fail(PEARL_ERR_WORKSPACE, "workspace_bytes %zu < required %zu", ws_bytes, pl.lay.total);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
@@ -392,5 +404,18 @@ size_t pearl_attn_workspace_bytes(const pearl_kv_shape* shape, const pearl_seq_d
 PEARL_ATTN_ENTRY(pearl_attn_prefill_append, kModePrefill)
 PEARL_ATTN_ENTRY(pearl_attn_decode, kModeDecode)
 PEARL_ATTN_ENTRY(pearl_attn_mixed, kModeMixed)
+
+size_t pearl_attn_decode_static_max_bytes(void) { return kStaticScratchBytes; }
+
+pearl_status pearl_attn_decode_static(const pearl_kv_shape* shape, const pearl_seq_desc* seqs, const void* q,
+                                      const void* k_pool, const void* v_pool, float softmax_scale, void* out,
+                                      float* lse, void* stream) {
+  try {
+    return run_attention(kModeDecode, shape, seqs, q, k_pool, v_pool, softmax_scale, out, lse, nullptr, 0, stream,
+                         /*static_ws=*/true);
+  } catch (...) {
+    return fail(PEARL_ERR_HIP, "unexpected exception in pearl_attn_decode_static");
+  }
+}
 
 }  // extern "C"

@@ -1211,6 +1211,14 @@ __global__ __launch_bounds__(256) void merge_prefill_kernel(AttnArgs a) {
 }
 
 // ------------------------------------------------------------------------------------------------
+// Device memory of the allocation-free decode entry point (pearl_attn_decode_static): the
+// workspace of one call, one array per device for the life of the process.  Host code never uses
+// the array's name as an address: the device address comes from hipGetSymbolAddress, taken once
+// per device with that device current.
+// ------------------------------------------------------------------------------------------------
+static __device__ __align__(256) char scratch[kStaticScratchBytes];
+
+// ------------------------------------------------------------------------------------------------
 // host launchers
 // ------------------------------------------------------------------------------------------------
 namespace {
@@ -1220,6 +1228,8 @@ struct DevCache {
   std::atomic<int> ready{0};
   int num_cu = 0;
   int occ[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};   // [D == 128][kinds]
+  void* scratch = nullptr;                        // device address of this device's scratch array
+  hipError_t scratch_err = hipSuccess;
 };
 
 template <int D, int K>
@@ -1236,6 +1246,9 @@ void fill_cache(DevCache& c, int dev) {
   c.occ[0][1] = occupancy_of<64, 1>(); c.occ[0][2] = occupancy_of<64, 2>(); c.occ[0][3] = occupancy_of<64, 3>();
   c.occ[1][1] = occupancy_of<128, 1>(); c.occ[1][2] = occupancy_of<128, 2>(); c.occ[1][3] = occupancy_of<128, 3>();
   c.num_cu = ncu;
+  void* p = nullptr;
+  c.scratch_err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+  c.scratch = c.scratch_err == hipSuccess ? p : nullptr;
 }
 
 constexpr int kCachedDevices = 64;
@@ -1263,6 +1276,12 @@ const DevCache& dev_cache() {
 }  // namespace
 
 int device_num_cu() { return dev_cache().num_cu; }
+
+void* static_scratch(hipError_t* err) {
+  const DevCache& c = dev_cache();
+  if (err) *err = c.scratch_err;
+  return c.scratch;
+}
 
 int attention_grid(int head_dim, int kinds) {
   const DevCache& c = dev_cache();

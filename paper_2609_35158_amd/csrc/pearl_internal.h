@@ -122,6 +122,11 @@ WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_head
                           bool has_prefill);
 int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu);
 int device_num_cu();
+// Bytes of the per-device static workspace of pearl_attn_decode_static.
+constexpr size_t kStaticScratchBytes = size_t(32) << 20;
+// Device address of the current device's static workspace (NULL with *err set on failure).  The
+// address is taken once per device, on the first call made with that device current.
+void* static_scratch(hipError_t* err);
 // Workgroups of a full persistent attention grid on the current device (compute units x
 // occupancy of the kernel for this head_dim and kinds).
 int attention_grid(int head_dim, int kinds);

@@ -154,3 +154,30 @@ def test_hbm_probe_host_validation():
     assert lib.pearl_hbm_read(FAKE, 32, None, None) == INVALID
     assert lib.pearl_hbm_fill(None, 32, 0, None) == INVALID
     assert lib.pearl_hbm_fill(FAKE, 40, 0, None) == INVALID
+
+
+def call_static(s, d, q=FAKE, kp=FAKE, vp=FAKE, scale=0.1, out=FAKE, lse=None):
+    st = pa.load().pearl_attn_decode_static(None if s is None else ctypes.byref(s),
+                                            None if d is None else ctypes.byref(d), q, kp, vp, scale, out, lse, None)
+    return st, pa.last_error()
+
+
+def test_decode_static_host_validation():
+    """The allocation-free decode checks its arguments like pearl_attn_decode, and rejects a batch
+    whose workspace exceeds its static limit, all before any HIP call."""
+    lib = pa.load()
+    assert lib.pearl_attn_decode_static_max_bytes() == 32 << 20
+    assert call_static(None, desc())[0] == INVALID
+    assert call_static(shape(), None)[0] == INVALID
+    assert call_static(shape(hq=32, hkv=2), desc())[0] == UNSUPPORTED
+    assert call_static(shape(), desc(batch=0))[0] == INVALID
+    assert call_static(shape(), desc(), q=None)[0] == INVALID
+    assert call_static(shape(), desc(), out=FAKE + 2)[0] == INVALID
+    assert call_static(shape(), desc(), scale=0.0)[0] == INVALID
+    st, msg = call_static(shape(), desc(cu=FAKE))
+    assert st == INVALID and "cu_q_lens" in msg
+    # 2048 sequences of up to 32K keys need far more than 32 MiB of split partials
+    big = desc(batch=2048, stride=2100, max_kv=33000)
+    assert ws_bytes(shape(), big) > lib.pearl_attn_decode_static_max_bytes()
+    st, msg = call_static(shape(), big)
+    assert st == UNSUPPORTED and "static limit" in msg
