@@ -161,7 +161,9 @@ def lengths_dev(torch, case):
 def make_step(torch, pa, case, mode):
     """Closure performing kv_append + attention for `case` through the C ABI with pre-built
     argument structs (lengths unchanged across steps, so the append rewrites the same slots with
-    the same bytes and every step does identical work)."""
+    the same bytes and every step does identical work).  A decode step is one
+    pearl_attn_decode_append call (the append fused into the decode launch); the append alone
+    (attention=False) is pearl_kv_append."""
     import ctypes
     from paper_2609_35158_amd import binding as bd
     lib = pa.load()
@@ -185,6 +187,15 @@ def make_step(torch, pa, case, mode):
     scale = ctypes.c_float(case.scale)
 
     def step(hook, attention=True, append=True):
+        if mode == "decode" and append and attention:
+            hook()
+            st = lib.pearl_attn_decode_append(sp, dp_a, case.q.data_ptr(), case.k_new.data_ptr(), case.v_new.data_ptr(),
+                                              case.k_pool.data_ptr(), case.v_pool.data_ptr(), scale, out.data_ptr(),
+                                              None, ws.data_ptr(), nbytes, stream)
+            lib.pearl_set_kernel_events(None, None)
+            if st:
+                raise bd.PearlError(st, "pearl_attn_decode_append", bd.last_error())
+            return
         if append:
             st = lib.pearl_kv_append(sp, dp_p, *app, stream)
             if st:
@@ -243,7 +254,7 @@ def time_append(torch, pa, step, steps):
 
 
 def time_graph_step(torch, pa, cases, steps, warmup):
-    """The same decode step (kv_append + decode) captured in a HIP graph, once per replica, and
+    """The same decode step (pearl_attn_decode_append) captured in a HIP graph, once per replica, and
     replayed: the library synchronises nothing and allocates nothing, so the whole step is
     capturable.  Returns ms per step."""
     import numpy as np
@@ -257,8 +268,8 @@ def time_graph_step(torch, pa, cases, steps, warmup):
 
     def step():
         for c, out in zip(cases, outs):
-            pa.kv_append(c.k_new, c.v_new, c.k_pool, c.v_pool, c.block_table, ctx, None, 1, max_kv)
-            pa.decode(c.q, c.k_pool, c.v_pool, c.block_table, ctx, max_kv, scale=c.scale, out=out, workspace=ws)
+            pa.decode_append(c.q, c.k_new, c.v_new, c.k_pool, c.v_pool, c.block_table, ctx, max_kv, scale=c.scale,
+                             out=out, workspace=ws)
 
     step()
     torch.cuda.synchronize()
@@ -878,7 +889,8 @@ def main():
         "config": {
             "workload": "qwen3-8b-decode: one attention layer, 32 q-heads / 8 kv-heads / d=128, bf16, "
                         "16-token pages, batch 64, cached context uniform [2048,16384] (seed 1), "
-                        "random page placement; step = kv_append + decode",
+                        "random page placement; step = kv_append + decode as one pearl_attn_decode_append call "
+                        "(zeroing prologue + decode kernel with the append, planning and split merge inside)",
             "batch": case.batch, "keys": int(case.kv_lens.sum()), "head_dim": 128,
             "num_q_heads": 32, "num_kv_heads": 8, "page_size": 16,
         },

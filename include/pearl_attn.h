@@ -156,6 +156,22 @@ pearl_status pearl_attn_decode(const pearl_kv_shape* shape, const pearl_seq_desc
                                void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * One decode step with its append: pearl_kv_append of this step's K/V rows (one per sequence)
+ * followed by pearl_attn_decode, with the same results bit for bit (outputs, LSE and both pools).
+ * A decode step always appends before it attends (paper, Background: the context grows by every
+ * generated token; section 4.3, Eq. 1: the per-step decode cost), so the two run as one launch
+ * sequence: the split holding each sequence's last page takes the new K/V straight from k_new /
+ * v_new and writes them into the pools itself.
+ *   k_new, v_new: bf16 [batch][num_kv_heads][head_dim] (read), 16-byte aligned;
+ *   k_pool, v_pool: written at position ctx_lens[b] of every sequence, read for attention;
+ *   the other arguments as for pearl_attn_decode (cu_q_lens must be NULL).
+ */
+pearl_status pearl_attn_decode_append(const pearl_kv_shape* shape, const pearl_seq_desc* seqs,
+                                      const void* q, const void* k_new, const void* v_new, void* k_pool,
+                                      void* v_pool, float softmax_scale, void* out, float* lse,
+                                      void* workspace, size_t workspace_bytes, void* stream);
+
+/*
  * Colocated mixed batch in one attention launch (paper, Motivation: chunked prefill batched
  * with decode; section 4.3, Eq. 1: prefill and decode share the GPU under colocation).  Each
  * sequence may have any number of new tokens (>= 0): sequences with exactly one new token take

@@ -4,9 +4,9 @@ behind a C ABI (include/pearl_attn.h).
 
 The Python layer only marshals arguments (see ``binding``); it has no compute fallback."""
 from .binding import (  # noqa: F401
-    LIB_PATH, PearlError, abi_version, decode, kv_append, kv_pack, kv_unpack, last_error, load, mixed,
+    LIB_PATH, PearlError, abi_version, decode, decode_append, kv_append, kv_pack, kv_unpack, last_error, load, mixed,
     prefill_append, workspace_bytes,
 )
 
-__all__ = ["kv_append", "kv_pack", "kv_unpack", "prefill_append", "decode", "mixed", "workspace_bytes",
+__all__ = ["kv_append", "kv_pack", "kv_unpack", "prefill_append", "decode", "decode_append", "mixed", "workspace_bytes",
            "abi_version", "last_error", "load", "PearlError", "LIB_PATH"]

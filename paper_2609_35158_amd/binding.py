@@ -43,7 +43,7 @@ EXPORTED = ("pearl_abi_version", "pearl_status_str", "pearl_last_error", "pearl_
             "pearl_attn_workspace_bytes", "pearl_attn_prefill_append", "pearl_attn_decode",
             "pearl_attn_mixed", "pearl_kv_pack", "pearl_kv_unpack", "pearl_set_kernel_events",
             "pearl_hbm_copy", "pearl_hbm_read", "pearl_hbm_fill", "pearl_attn_decode_static",
-            "pearl_attn_decode_static_max_bytes")
+            "pearl_attn_decode_static_max_bytes", "pearl_attn_decode_append")
 
 
 def load(path: str = LIB_PATH):
@@ -78,6 +78,11 @@ def load(path: str = LIB_PATH):
         f.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                       ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                       ctypes.c_size_t, ctypes.c_void_p]
+    lib.pearl_attn_decode_append.restype = ctypes.c_int
+    lib.pearl_attn_decode_append.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p,
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_float,
+                                             ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                                             ctypes.c_void_p]
     lib.pearl_attn_decode_static.restype = ctypes.c_int
     lib.pearl_attn_decode_static.argtypes = [P(KvShape), P(SeqDesc), ctypes.c_void_p, ctypes.c_void_p,
                                              ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p, ctypes.c_void_p,
@@ -271,6 +276,44 @@ def decode(q, k_pool, v_pool, block_table, ctx_lens, max_kv_len, scale=None, ret
     """Single-token decode for every sequence (pearl_attn_decode); q is [batch][H_q][d]."""
     return _attention("pearl_attn_decode", q, k_pool, v_pool, block_table, ctx_lens, None,
                       1, max_kv_len, scale, return_lse, out, lse, workspace)
+
+
+def decode_append(q, k_new, v_new, k_pool, v_pool, block_table, ctx_lens, max_kv_len, scale=None,
+                  return_lse=False, out=None, lse=None, workspace=None):
+    """One decode step with its append (pearl_attn_decode_append): k_new / v_new [batch][H_kv][d]
+    are written at position ctx_lens[b] of every sequence, which then attends over ctx_lens[b] + 1
+    keys; q is [batch][H_q][d]."""
+    for t, n in ((q, "q"), (k_new, "k_new"), (v_new, "v_new"), (k_pool, "k_pool"), (v_pool, "v_pool")):
+        _need(t, n, torch.bfloat16)
+    if q.dim() != 3:
+        raise ValueError("q must be [batch][num_q_heads][head_dim]")
+    batch, H_q, d = q.shape
+    if tuple(k_new.shape) != (batch, k_pool.shape[1], d) or tuple(v_new.shape) != tuple(k_new.shape):
+        raise ValueError("k_new and v_new must be [batch][num_kv_heads][head_dim]")
+    desc = make_desc(block_table, ctx_lens, None, batch, 1, max_kv_len)
+    shape = make_shape(H_q, k_pool)
+    if out is None:
+        out = torch.empty_like(q)
+    _need(out, "out", torch.bfloat16)
+    if return_lse and lse is None:
+        lse = torch.empty((batch, H_q), dtype=torch.float32, device=q.device)
+    if lse is not None:
+        _need(lse, "lse", torch.float32)
+    if workspace is None:
+        nbytes = load().pearl_attn_workspace_bytes(ctypes.byref(shape), ctypes.byref(desc))
+        if nbytes == 0:
+            raise PearlError(1, "pearl_attn_workspace_bytes", last_error())
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device=q.device)
+    else:
+        _need(workspace, "workspace", torch.uint8)
+    if scale is None:
+        scale = 1.0 / float(d) ** 0.5
+    st = load().pearl_attn_decode_append(ctypes.byref(shape), ctypes.byref(desc), q.data_ptr(), k_new.data_ptr(),
+                                         v_new.data_ptr(), k_pool.data_ptr(), v_pool.data_ptr(), float(scale),
+                                         out.data_ptr(), _ptr(lse), workspace.data_ptr(), workspace.numel(),
+                                         _stream())
+    _check(st, "pearl_attn_decode_append")
+    return (out, lse) if (return_lse or lse is not None) else out
 
 
 def decode_static(q, k_pool, v_pool, block_table, ctx_lens, max_kv_len, scale=None, return_lse=False,

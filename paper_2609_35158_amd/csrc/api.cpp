@@ -125,9 +125,12 @@ Plan make_plan(const pearl_kv_shape* s, const pearl_seq_desc* q, int mode) {
 
 // static_ws: use the library's static per-device workspace (pearl_attn_decode_static) instead of
 // the caller's ws / ws_bytes; its address is looked up only after every host check has passed.
+// k_new / v_new (decode only, both or neither): append the new tokens' K/V first, as
+// pearl_kv_append would; decode planned in-kernel does it inside the attention kernel.
 pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_desc* q, const void* qp,
                            const void* k_pool, const void* v_pool, float scale, void* out, float* lse,
-                           void* ws, size_t ws_bytes, void* stream, bool static_ws = false) {
+                           void* ws, size_t ws_bytes, void* stream, bool static_ws = false,
+                           const void* k_new = nullptr, const void* v_new = nullptr) {
   g_err[0] = 0;
   pearl_status st = check_shape(s);
   if (st != PEARL_OK) return st;
@@ -136,6 +139,9 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   if (mode == kModeDecode && q->cu_q_lens)
     return fail(PEARL_ERR_INVALID_ARG, "pearl_attn_decode requires cu_q_lens == NULL (one token per sequence)");
   if (!qp || !k_pool || !v_pool || !out) return fail(PEARL_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be non-NULL");
+  if ((k_new == nullptr) != (v_new == nullptr)) return fail(PEARL_ERR_INVALID_ARG, "k_new and v_new must both be given");
+  if (k_new && (!aligned16(k_new) || !aligned16(v_new)))
+    return fail(PEARL_ERR_INVALID_ARG, "k_new and v_new must be 16-byte aligned");
   if (!ws && !static_ws) return fail(PEARL_ERR_WORKSPACE, "workspace is NULL");
   if (!aligned16(qp) || !aligned16(k_pool) || !aligned16(v_pool) || !aligned16(out))
     return fail(PEARL_ERR_INVALID_ARG, "q, k_pool, v_pool and out must be 16-byte aligned");
@@ -163,8 +169,21 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
     return fail(PEARL_ERR_WORKSPACE, "workspace_bytes %zu < required %zu", ws_bytes, pl.lay.total);
   hipStream_t hs = reinterpret_cast<hipStream_t>(stream);
   char* w = static_cast<char*>(ws);
-  hipError_t e = launch_plan(pl.p, q->ctx_lens, q->cu_q_lens, ws, pl.lay, hs);
-  if (e != hipSuccess) return fail(PEARL_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+  // decode batches up to kDecPlanMaxSeqs are planned inside the attention kernel, which also
+  // merges the splits; everything else is planned by plan_kernel and merged by the merge kernels
+  const bool dec_in_kernel = mode == kModeDecode && q->batch <= kDecPlanMaxSeqs;
+  hipError_t e = hipSuccess;
+  if (k_new && !dec_in_kernel) {
+    e = launch_kv_append(static_cast<const uint16_t*>(k_new), static_cast<const uint16_t*>(v_new),
+                         static_cast<uint16_t*>(const_cast<void*>(k_pool)), static_cast<uint16_t*>(const_cast<void*>(v_pool)),
+                         q->block_table, q->bt_stride, q->ctx_lens, nullptr, q->batch, 1, s->num_kv_heads, s->head_dim,
+                         s->num_pages, q->total_q, hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "kv_append launch: %s", hipGetErrorString(e));
+  }
+  if (!dec_in_kernel) {
+    e = launch_plan(pl.p, q->ctx_lens, q->cu_q_lens, ws, pl.lay, hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "plan launch: %s", hipGetErrorString(e));
+  }
   AttnArgs a;
   a.q = static_cast<const uint16_t*>(qp);
   a.k_pool = static_cast<const uint16_t*>(k_pool);
@@ -181,6 +200,11 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   a.pre_jobs = reinterpret_cast<const int4*>(w + pl.lay.pre_jobs);
   a.part_pre_o = reinterpret_cast<float*>(w + pl.lay.part_pre_o);
   a.part_pre_ml = reinterpret_cast<float*>(w + pl.lay.part_pre_ml);
+  a.split_cnt = reinterpret_cast<int32_t*>(w + pl.lay.split_cnt);
+  a.k_new = dec_in_kernel ? static_cast<const uint16_t*>(k_new) : nullptr;
+  a.v_new = dec_in_kernel ? static_cast<const uint16_t*>(v_new) : nullptr;
+  a.k_pool_w = static_cast<uint16_t*>(const_cast<void*>(k_pool));
+  a.v_pool_w = static_cast<uint16_t*>(const_cast<void*>(v_pool));
   a.bt_stride = q->bt_stride;
   a.num_pages = s->num_pages;
   a.num_q_heads = s->num_q_heads;
@@ -189,14 +213,28 @@ pearl_status run_attention(int mode, const pearl_kv_shape* s, const pearl_seq_de
   a.tokens_per_tile = pl.p.tokens_per_tile;
   a.scale_log2 = scale * 1.4426950408889634f;
   const int64_t max_items = (pl.lay.max_pre + pl.lay.max_dec) * s->num_kv_heads;
+  if (dec_in_kernel) {
+    e = launch_decode_prologue(a, q->batch, hs);
+    if (e != hipSuccess) return fail(PEARL_ERR_HIP, "decode prologue launch: %s", hipGetErrorString(e));
+  }
   e = record_before(hs);
   if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
-  const int kinds = mode == kModePrefill ? 1 : (mode == kModeDecode ? 2 : 3);
-  e = launch_attention(a, s->head_dim, kinds, max_items, (int)pl.lay.max_pre, hs);
+  if (dec_in_kernel) {
+    DecPlanArgs d;
+    d.ctx_lens = q->ctx_lens;
+    d.batch = q->batch;
+    d.max_kv_len = q->max_kv_len;
+    d.pps_min = pl.p.pages_per_split;
+    d.max_dec = (int)pl.lay.max_dec;
+    e = launch_decode(a, d, s->head_dim, pl.lay.max_dec * s->num_kv_heads, hs);
+  } else {
+    const int kinds = mode == kModePrefill ? 1 : (mode == kModeDecode ? 2 : 3);
+    e = launch_attention(a, s->head_dim, kinds, max_items, (int)pl.lay.max_pre, hs);
+  }
   if (e != hipSuccess) return fail(PEARL_ERR_HIP, "attention launch: %s", hipGetErrorString(e));
   e = record_after(hs);
   if (e != hipSuccess) return fail(PEARL_ERR_HIP, "timing event: %s", hipGetErrorString(e));
-  if (mode != kModePrefill && pl.lay.max_dec > 0) {
+  if (!dec_in_kernel && mode != kModePrefill && pl.lay.max_dec > 0) {
     e = launch_merge(a, s->head_dim, q->batch, hs);
     if (e != hipSuccess) return fail(PEARL_ERR_HIP, "merge launch: %s", hipGetErrorString(e));
   }
@@ -268,6 +306,7 @@ WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_head
   l.pre_jobs = off; off = align256(off + sizeof(int4) * (size_t)l.pre_jobs_cap);
   l.part_pre_o = off; off = align256(off + sizeof(float) * (size_t)l.pre_slots * kRowsPerTile * head_dim);
   l.part_pre_ml = off; off = align256(off + sizeof(float) * 2 * (size_t)l.pre_slots * kRowsPerTile);
+  l.split_cnt = off; off = align256(off + sizeof(int32_t) * (size_t)batch * num_kv_heads);
   l.total = off;
   return l;
 }
@@ -404,6 +443,22 @@ size_t pearl_attn_workspace_bytes(const pearl_kv_shape* shape, const pearl_seq_d
 PEARL_ATTN_ENTRY(pearl_attn_prefill_append, kModePrefill)
 PEARL_ATTN_ENTRY(pearl_attn_decode, kModeDecode)
 PEARL_ATTN_ENTRY(pearl_attn_mixed, kModeMixed)
+
+pearl_status pearl_attn_decode_append(const pearl_kv_shape* shape, const pearl_seq_desc* seqs, const void* q,
+                                      const void* k_new, const void* v_new, void* k_pool, void* v_pool,
+                                      float softmax_scale, void* out, float* lse, void* workspace,
+                                      size_t workspace_bytes, void* stream) {
+  try {
+    if (!k_new || !v_new) {
+      g_err[0] = 0;
+      return fail(PEARL_ERR_INVALID_ARG, "k_new and v_new must be non-NULL");
+    }
+    return run_attention(kModeDecode, shape, seqs, q, k_pool, v_pool, softmax_scale, out, lse, workspace,
+                         workspace_bytes, stream, false, k_new, v_new);
+  } catch (...) {
+    return fail(PEARL_ERR_HIP, "unexpected exception in pearl_attn_decode_append");
+  }
+}
 
 size_t pearl_attn_decode_static_max_bytes(void) { return kStaticScratchBytes; }
 

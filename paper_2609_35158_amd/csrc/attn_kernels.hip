@@ -795,19 +795,29 @@ template <int D> struct VTile {
 };
 
 
-template <int D>
+// The new token's K/V row of a fused append-and-decode: logical page `page`, slot `slot`, taken
+// from the caller's k_new / v_new rows instead of the pool (page -1: none).
+struct NewRow {
+  int page, slot;
+  const uint16_t* k;
+  const uint16_t* v;
+};
+
+// kNew: the item may hold the new row (decode_kernel); otherwise nr is ignored.
+template <int D, bool kNew>
 __device__ __forceinline__ void decode_issue(const AttnArgs& a, int phys_a, int phys_b, bool pb_ok, int pa,
-                                             int g, int kv, DecodeK<D>& K, char* vdst) {
+                                             int g, int kv, DecodeK<D>& K, char* vdst, const NewRow& nr) {
   using VT = VTile<D>;
   const int lane = threadIdx.x & 63, gi = lane >> 4, hh = lane & 15;
   const size_t head_stride = (size_t)kPage * D;
   const size_t ga = ((size_t)phys_a * a.num_kv_heads + g) * head_stride;
   const size_t gb = ((size_t)phys_b * a.num_kv_heads + g) * head_stride;
+  const bool new_a = kNew && pa == nr.page && hh == nr.slot, new_b = kNew && pa + 1 == nr.page && hh == nr.slot;
 #pragma unroll
   for (int kb = 0; kb < DecodeK<D>::KB; ++kb) {
     const int off = hh * D + 32 * kb + 8 * gi;
-    K.ka[kb] = ld16(a.k_pool + ga + off);
-    K.kb[kb] = ld16(a.k_pool + gb + off);
+    K.ka[kb] = ld16(new_a ? nr.k + 32 * kb + 8 * gi : a.k_pool + ga + off);
+    K.kb[kb] = ld16(new_b ? nr.k + 32 * kb + 8 * gi : a.k_pool + gb + off);
   }
   const uint16_t* zero = reinterpret_cast<const uint16_t*>(a.ws_hdr + kHdrZero);
 #pragma unroll
@@ -817,7 +827,8 @@ __device__ __forceinline__ void decode_issue(const AttnArgs& a, int phys_a, int 
     const int c = slot_c ^ VT::swz(r);              // global chunk stored there
     const int pg = r >> 4, key = r & 15;            // pg is the same for every lane of a given i
     const bool ok = (pg == 0 || pb_ok) && (pa + pg) * kPage + key < kv;
-    const uint16_t* src = ok ? a.v_pool + (pg ? gb : ga) + key * D + c * 8 : zero;
+    const bool is_new = kNew && pa + pg == nr.page && key == nr.slot;
+    const uint16_t* src = ok ? (is_new ? nr.v + c * 8 : a.v_pool + (pg ? gb : ga) + key * D + c * 8) : zero;
     lds_dma16(src, vdst + i * 1024);
   }
 }
@@ -899,25 +910,142 @@ __device__ __forceinline__ PairPages pair_pages(ConstI32Ptr bt_row, int p_begin,
   return pp;
 }
 
+// One decode work item as the kernels see it: sequence b (its new token is row q_row of q/out),
+// kv attended keys, split `split` of n_splits (pps pages each), kv-head g; the partials of a
+// multi-split sequence go to slots slot_base + split.
+struct DecItem {
+  int b, split, g, q_row, kv, n_splits, slot_base;
+};
+
+// Split merge inside the attention kernel.  Every split of a multi-split (sequence, kv-head) pair
+// stores its partial (o~, m, l) with device-scope stores (written through to the level every XCD
+// reads) and moves on.  One item later, once every thread of the workgroup has drained its memory
+// operations (so those stores are acknowledged) and passed a barrier, one thread counts the split
+// in with a device-scope atomic in split_cnt[b][g] (zeroed before the launch); the workgroup that
+// brings the count to n_splits merges the pair (merge_in_kernel).  No release fence is issued: on
+// this chip its L2 write-back costs far more than the merge launch it replaces, and deferring the
+// count-in by one item keeps the store acknowledgements off the critical path.
+//
+// merge_in_kernel: wave w merges q-head w of the group (G <= NW) from the partials, read with
+// device-scope loads (which do not hit stale cache lines):
+//   o = sum_s 2^(m_s - m*) o~_s / sum_s 2^(m_s - m*) l_s,   lse = (m* + log2 l*) ln 2.
+// Lane s holds split s's (m, l); every lane holds D/64 dims of o.  The first block of o~ loads is
+// issued together with the (m, l) loads, so up to kMergeBlock splits cost one memory round trip.
+constexpr int kMergeBlock = 8;
+
+template <int D, int NW>
+__device__ __forceinline__ void merge_in_kernel(const AttnArgs& a, const DecItem& it) {
+  const int G = a.group, H_q = a.num_q_heads;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  if (w >= G) return;
+  constexpr int PER = D / 64;
+  constexpr int U = kMergeBlock;
+  const int hq = it.g * G + w;
+  const size_t base = (size_t)it.slot_base;
+  const int ns = it.n_splits;
+  auto ld = [](const float* p) { return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT); };
+  auto o_ptr = [&](int sp) { return a.part_o + ((base + sp) * H_q + hq) * D + lane * PER; };
+  // (m, l) of the first 64 splits and o~ of the first U, all in flight together
+  float m0 = -INFINITY, l0 = 0.f;
+  if (lane < ns) {
+    m0 = ld(&a.part_ml[2 * ((base + lane) * H_q + hq)]);
+    l0 = ld(&a.part_ml[2 * ((base + lane) * H_q + hq) + 1]);
+  }
+  float v0[U][PER];
+#pragma unroll
+  for (int u = 0; u < U; ++u) {
+    const float* po = o_ptr(min(u, ns - 1));      // past the end: reload the last split, weight 0
+#pragma unroll
+    for (int i = 0; i < PER; ++i) v0[u][i] = ld(po + i);
+  }
+  float M = m0;
+  for (int s0 = 64; s0 < ns; s0 += 64)
+    if (s0 + lane < ns) M = fmaxf(M, ld(&a.part_ml[2 * ((base + s0 + lane) * H_q + hq)]));
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off));
+  float acc[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) acc[i] = 0.f;
+  float L = 0.f;
+  for (int s0 = 0; s0 < ns; s0 += 64) {
+    const int cnt = min(64, ns - s0);
+    float f = 0.f;
+    if (lane < cnt) {
+      const size_t pidx = (base + s0 + lane) * H_q + hq;
+      const float m = s0 == 0 ? m0 : ld(&a.part_ml[2 * pidx]);
+      const float l = s0 == 0 ? l0 : ld(&a.part_ml[2 * pidx + 1]);
+      f = fexp2(m - M);
+      L += f * l;
+    }
+    for (int j = 0; j < cnt; j += U) {
+      float v[U][PER], fj[U];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        const int jj = min(j + u, cnt - 1);
+        const float wgt = __shfl(f, jj);
+        fj[u] = j + u < cnt ? wgt : 0.f;
+        if (s0 == 0 && j == 0) {
+#pragma unroll
+          for (int i = 0; i < PER; ++i) v[u][i] = v0[u][i];
+        } else {
+          const float* po = o_ptr(s0 + jj);
+#pragma unroll
+          for (int i = 0; i < PER; ++i) v[u][i] = ld(po + i);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < U; ++u)
+#pragma unroll
+        for (int i = 0; i < PER; ++i) acc[i] += fj[u] * v[u][i];
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) L += __shfl_xor(L, off);
+  const float inv = 1.0f / L;
+  uint16_t* orow = a.out + ((size_t)it.q_row * H_q + hq) * D + lane * PER;
+#pragma unroll
+  for (int i = 0; i < PER; ++i) orow[i] = bf16_bits(acc[i] * inv);
+  if (lane == 0 && a.lse) a.lse[(size_t)it.q_row * H_q + hq] = (M + flog2(L)) * kLn2;
+}
+
+// Counts a finished split in (thread 0; the caller has made its partial stores acknowledged and
+// passed a barrier); returns 1 to the thread if this was the pair's last split.
+__device__ __forceinline__ int count_split_in(const AttnArgs& a, const DecItem& it) {
+  const int prev = __hip_atomic_fetch_add(&a.split_cnt[it.b * a.num_kv_heads + it.g], 1, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+  return prev == it.n_splits - 1;
+}
+
+// lgkmcnt(0) with the other counters left alone (gfx9 encoding)
+#define PEARL_LGKMCNT0 0xC07F
+
 // One pipeline step: issue the next pair (K into k_next, V by DMA into v_next), then consume the
 // current pair from k_cur / v_cur.  The step is branch-free: a wave with no further pair re-issues
 // its current pair (L2 hits, results unused), so every step leaves exactly one pair in flight.
 // The two V buffers are __restrict__ parameters of this one function, so the compiler knows the
 // reads of v_cur cannot alias the DMA still writing v_next and waits only for the current pair.
-template <int D>
+template <int D, bool kNew>
 __device__ __forceinline__ void decode_step(const AttnArgs& a, const PairPages& cur, const PairPages& nxt, int g,
                                             int kv, DecodeK<D>& k_next, const DecodeK<D>& k_cur,
                                             char* __restrict__ v_next, const char* __restrict__ v_cur,
-                                            const bf16x8* qop, f32x4* oacc, float& m_run, float& l_run) {
+                                            const bf16x8* qop, f32x4* oacc, float& m_run, float& l_run,
+                                            const NewRow& nr) {
   constexpr int PAIR_LOADS = 2 * DecodeK<D>::KB + VTile<D>::NDMA;   // vector-memory ops per pair
-  decode_issue<D>(a, nxt.phys_a, nxt.phys_b, nxt.pb_ok, nxt.pa, g, kv, k_next, v_next);
+  decode_issue<D, kNew>(a, nxt.phys_a, nxt.phys_b, nxt.pb_ok, nxt.pa, g, kv, k_next, v_next, nr);
   __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));              // the current pair has landed
   decode_consume<D>(a, k_cur, cur.pa, cur.pb_ok, kv, qop, oacc, m_run, l_run, v_cur);
 }
 
-template <int D, int NW>
-__device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split, int g, int pps, char* vbufA,
-                                             char* vbufB) {
+// kMergeHere: a multi-split (sequence, kv-head) is merged inside the attention kernel by the split
+// that finishes last (see the end of decode_split); otherwise merge_kernel runs after the launch.
+// kMergeHere: `pend` is this workgroup's previous multi-split item, not yet counted in (b < 0:
+// none); it is counted in (and merged if last) here, and becomes this item if it has splits.
+// s_flag: an LDS word.
+// before_end: called by every thread just before the item's closing barrier (decode_kernel
+// decodes its next item there, so the claim's latency hides behind this item).
+template <int D, int NW, bool kMergeHere, typename BeforeEnd>
+__device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& it, int pps, char* vbufA,
+                                             char* vbufB, DecItem& pend, int* s_flag, BeforeEnd before_end) {
   constexpr int NT = NW * 64;
   using VT = VTile<D>;
   constexpr int MB = D / 16;
@@ -925,9 +1053,9 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
   constexpr int PAIR_LOADS = 2 * KB + VT::NDMA;    // vector-memory instructions issued per pair
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
   const int gi = lane >> 4, hh = lane & 15;
-  const SeqInfo si = a.seqinfo[b];
+  const int b = it.b, split = it.split, g = it.g;
   const int G = a.group, H_q = a.num_q_heads;
-  const int kv = si.ctx_len + si.q_len;
+  const int kv = it.kv;
   const int n_pages = (kv + kPage - 1) / kPage;
   const int p_begin = split * pps;
   const int p_end = min(p_begin + pps, n_pages);
@@ -940,7 +1068,7 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
 
   bf16x8 qop[KB];
   {
-    const uint16_t* qrow = a.q + ((size_t)si.q_start * H_q + g * G + (head_ok ? hh : 0)) * D + 8 * gi;
+    const uint16_t* qrow = a.q + ((size_t)it.q_row * H_q + g * G + (head_ok ? hh : 0)) * D + 8 * gi;
 #pragma unroll
     for (int kb = 0; kb < KB; ++kb) {
       const bf16x8 v = as_bf16x8(ld16(qrow + 32 * kb));
@@ -950,7 +1078,18 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
   DecodeK<D> kA, kB;
   const int last = n_pairs - 1;
   PairPages cur = pair_pages(bt_row, p_begin, p_end, min(w, last), a.num_pages);
-  if (w < n_pairs) decode_issue<D>(a, cur.phys_a, cur.phys_b, cur.pb_ok, cur.pa, g, kv, kA, vb0);
+  // fused append (decode kernel with k_new): the split holding the sequence's last page takes the
+  // new token's K/V from k_new / v_new; its last wave writes them into the pools once the item's
+  // reads are done (a write whose page id is out of range is skipped, as pearl_kv_append does).
+  // No other item reads that row.
+  NewRow nr{-1, 0, a.k_pool, a.v_pool};            // no new row (valid pointers, never selected)
+  if constexpr (kMergeHere) {
+    if (a.k_new && split == it.n_splits - 1) {
+      const size_t row = ((size_t)it.q_row * a.num_kv_heads + g) * D;
+      nr = NewRow{(kv - 1) / kPage, (kv - 1) % kPage, a.k_new + row, a.v_new + row};
+    }
+  }
+  if (w < n_pairs) decode_issue<D, kMergeHere>(a, cur.phys_a, cur.phys_b, cur.pb_ok, cur.pa, g, kv, kA, vb0, nr);
   f32x4 oacc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) oacc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -961,14 +1100,24 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
   for (int pi = w; pi < n_pairs; pi += 2 * NW) {
     const int pj = pi + NW, pk = pj + NW;
     const PairPages n2 = pk < n_pairs ? pair_pages(bt_row, p_begin, p_end, pk, a.num_pages) : nxt;
-    decode_step<D>(a, cur, nxt, g, kv, kB, kA, vb1, vb0, qop, oacc, m_run, l_run);
+    decode_step<D, kMergeHere>(a, cur, nxt, g, kv, kB, kA, vb1, vb0, qop, oacc, m_run, l_run, nr);
     if (pj >= n_pairs) break;
     const PairPages n3 = pk + NW < n_pairs ? pair_pages(bt_row, p_begin, p_end, pk + NW, a.num_pages) : n2;
-    decode_step<D>(a, nxt, n2, g, kv, kA, kB, vb0, vb1, qop, oacc, m_run, l_run);
+    decode_step<D, kMergeHere>(a, nxt, n2, g, kv, kA, kB, vb0, vb1, qop, oacc, m_run, l_run, nr);
     cur = n2;
     nxt = n3;
   }
   __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));      // drain the trailing re-issued pair
+  // the new row's bytes and page id are loaded now, to be stored once the LDS merge below has
+  // waited for them
+  const bool writer = kMergeHere && nr.page >= 0 && w == NW - 1 && lane < D / 8;
+  u32x4 new_k = u32x4{0u, 0u, 0u, 0u}, new_v = new_k;
+  int new_page = -1;
+  if (writer) {
+    new_k = ld16(nr.k + 8 * lane);
+    new_v = ld16(nr.v + 8 * lane);
+    new_page = bt_row[nr.page];
+  }
   // each head's four lane groups hold different keys: sum their l
   l_run += __shfl_xor(l_run, 16);
   l_run += __shfl_xor(l_run, 32);
@@ -986,7 +1135,22 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
     if (gi == 0) { mm[w * 8 + hh] = m_run; ml[w * 8 + hh] = l_run; }
   }
   __syncthreads();
-  const int n_splits = si.kind >> 4;
+  const int n_splits = it.n_splits;
+  // the previous item's partial stores: every thread drained its memory operations above
+  // (vmcnt(0)) before the barrier, so they are acknowledged.  The count-in's result is used only
+  // after the output loop, so its latency hides behind that loop.
+  int last_in = 0;
+  if constexpr (kMergeHere) {
+    // the new row's loads have completed (the barriers above waited for them); saying so here lets
+    // its stores below go out before the partial stores without any later wait reaching past them
+    __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
+    if (threadIdx.x == 0 && pend.b >= 0) last_in = count_split_in(a, pend);
+    if (writer && new_page >= 0 && new_page < a.num_pages) {
+      const size_t dst = (((size_t)new_page * a.num_kv_heads + g) * kPage + nr.slot) * D + 8 * lane;
+      *reinterpret_cast<u32x4*>(a.k_pool_w + dst) = new_k;
+      *reinterpret_cast<u32x4*>(a.v_pool_w + dst) = new_v;
+    }
+  }
   for (int t = threadIdx.x; t < G * D; t += NT) {
     const int head = t / D, dim = t - head * D;
     float M = -INFINITY;
@@ -1001,15 +1165,35 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, int b, int split
     }
     const int hq = g * G + head;
     if (n_splits == 1) {
-      a.out[((size_t)si.q_start * H_q + hq) * D + dim] = bf16_bits(o / L);
-      if (dim == 0 && a.lse) a.lse[(size_t)si.q_start * H_q + hq] = (M + flog2(L)) * kLn2;
+      a.out[((size_t)it.q_row * H_q + hq) * D + dim] = bf16_bits(o / L);
+      if (dim == 0 && a.lse) a.lse[(size_t)it.q_row * H_q + hq] = (M + flog2(L)) * kLn2;
     } else {
-      const size_t pidx = (size_t)(a.split_base[b] + split) * H_q + hq;
-      a.part_o[pidx * D + dim] = o;
-      if (dim == 0) { a.part_ml[2 * pidx] = M; a.part_ml[2 * pidx + 1] = L; }
+      const size_t pidx = (size_t)(it.slot_base + split) * H_q + hq;
+      if constexpr (kMergeHere) {
+        // device-scope stores: written through to the level where every XCD reads them
+        __hip_atomic_store(&a.part_o[pidx * D + dim], o, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (dim == 0) {
+          __hip_atomic_store(&a.part_ml[2 * pidx], M, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          __hip_atomic_store(&a.part_ml[2 * pidx + 1], L, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+      } else {
+        a.part_o[pidx * D + dim] = o;
+        if (dim == 0) { a.part_ml[2 * pidx] = M; a.part_ml[2 * pidx + 1] = L; }
+      }
     }
   }
-  __syncthreads();
+  before_end();
+  if constexpr (kMergeHere) {
+    if (threadIdx.x == 0) *s_flag = last_in;
+    // the LDS scratch has been read (the next item's copies overwrite it) and s_flag written; the
+    // stores just issued stay in flight (a plain barrier, without the release fence's vmcnt(0))
+    __builtin_amdgcn_s_waitcnt(PEARL_LGKMCNT0);
+    __asm__ volatile("s_barrier" ::: "memory");
+    if (*s_flag) merge_in_kernel<D, NW>(a, pend);
+    pend = n_splits > 1 ? it : DecItem{-1, 0, 0, 0, 0, 0, 0};
+  } else {
+    __syncthreads();
+  }
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -1091,13 +1275,256 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
     } else {
       if constexpr ((kKinds & 2) != 0) {
         const int2 en = a.entries[max_pre + (e - n_pre)];
-        decode_split<D, NW>(a, en.x, en.y, g, pps, vbufA, vbufB);
+        const SeqInfo si = a.seqinfo[en.x];
+        const DecItem it{en.x, en.y, g, si.q_start, si.ctx_len + si.q_len, si.kind >> 4, a.split_base[en.x]};
+        DecItem none{-1, 0, 0, 0, 0, 0, 0};
+        decode_split<D, NW, false>(a, it, pps, vbufA, vbufB, none, nullptr, [] {});
       }
     }
     __syncthreads();
     slot ^= 1;
     item = s_item[slot];
   }
+}
+
+// ------------------------------------------------------------------------------------------------
+// Decode-only batches of up to kDecPlanMaxSeqs sequences are planned inside the attention kernel:
+// every workgroup reads the lengths and builds the same work list in LDS (the same split sizing
+// and longest-first order as plan_kernel), so a decode call is one zeroing launch and this kernel,
+// with the split merge done by the last split of each (sequence, kv-head) (merge_in_kernel).
+// ------------------------------------------------------------------------------------------------
+constexpr int kDecPlanChunks = kDecPlanMaxSeqs / kThreads;
+static_assert(kDecPlanChunks * kThreads == kDecPlanMaxSeqs, "plan chunks");
+
+struct DecPlanLds {
+  int kv[kDecPlanMaxSeqs];                 // keys attended per sequence (context + the new token)
+  int full_pre[kDecPlanMaxSeqs + 1];       // exclusive prefix sums of full splits
+  int split_pre[kDecPlanMaxSeqs + 1];      // exclusive prefix sums of all splits (partial slot bases)
+  int order[kDecPlanMaxSeqs];              // sequences with a short last split, longest class first
+  int wsum[2][kWaves];
+  int cls_cnt[kDecPlanChunks][kWaves][kPartBuckets];
+  int cls_off[kDecPlanChunks][kWaves][kPartBuckets];   // first position of (chunk, wave, class) in order
+  unsigned long long pages;
+  int err, pps, n_full, n_items;
+};
+
+// Validates the lengths against the host bounds (any violation: no work, error 1) and builds the
+// list; splits beyond the workspace's partial slots give no work and error 2.  Ends with a barrier.
+// Sequences are taken kThreads at a time (chunks); a batch of at most kThreads sequences runs one.
+__device__ __forceinline__ void decode_plan(const AttnArgs& a, const DecPlanArgs& d, DecPlanLds& P) {
+  constexpr int C = kDecPlanChunks;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int B = d.batch, H = a.num_kv_heads;
+  const int nch = (B + kThreads - 1) / kThreads;    // chunks holding sequences (<= C)
+  if (tid == 0) { P.pages = 0; P.err = 0; }
+  int pages[C];
+  bool bad = false;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int b = c * kThreads + tid;
+    pages[c] = 0;
+    if (b < B) {
+      const int ctx = d.ctx_lens[b];
+      const long long kv = (long long)ctx + 1;
+      if (ctx < 0 || kv > d.max_kv_len || (kv + kPage - 1) / kPage > a.bt_stride) {
+        bad = true;
+      } else {
+        pages[c] = (int)((kv + kPage - 1) / kPage);
+        P.kv[b] = (int)kv;
+      }
+    }
+  }
+  unsigned long long wsum = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    unsigned sum = pages[c];                        // 64 sequences of < 2^21 pages
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) sum += __shfl_xor(sum, off);
+    wsum += sum;
+  }
+  const bool wave_bad = __any(bad);
+  __syncthreads();                                  // P.pages and P.err are initialised
+  if (lane == 0) {
+    atomicAdd(&P.pages, wsum);
+    if (wave_bad) atomicOr(&P.err, 1);
+  }
+  __syncthreads();
+  if (tid == 0) {
+    // pages per split: about kDecItemsPerCU items per compute unit, a multiple of 16, at least the
+    // host's bound, at least kDecLongSplitPages while that leaves 2 items per compute unit, at
+    // most kMaxPagesPerSplit (the rule plan_kernel applies)
+    long long pps = d.pps_min;
+    if (P.pages > 0) {
+      const long long units = (long long)P.pages * H;
+      const long long per = (long long)kPlanComputeUnits * kDecItemsPerCU;
+      const long long want = (units + per - 1) / per;
+      const long long two = (units + 2LL * kPlanComputeUnits - 1) / (2LL * kPlanComputeUnits);
+      pps = max(pps, (want + 15) / 16 * 16);
+      pps = max(pps, min((long long)kDecLongSplitPages, (two + 15) / 16 * 16));
+      pps = min(pps, (long long)max(d.pps_min, kMaxPagesPerSplit));
+    }
+    P.pps = (int)pps;
+  }
+  __syncthreads();
+  const int pps = P.pps;
+  const int err = P.err;
+  if (err) {
+#pragma unroll
+    for (int c = 0; c < C; ++c) pages[c] = 0;
+  }
+  const float inv_pps = (float)kPartBuckets / (float)pps;
+  int cls[C], rank[C];
+#pragma unroll
+  for (int c = 0; c < C; ++c) { cls[c] = -1; rank[c] = 0; }
+  int carry_f = 0, carry_s = 0;
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    if (c >= nch) break;                            // uniform
+    const int b = c * kThreads + tid;
+    const int nf = pages[c] / pps, rest = pages[c] - nf * pps;
+    const int ns = nf + (rest > 0);
+    cls[c] = rest > 0 ? part_bucket(rest, inv_pps) : -1;
+    int incl_f = nf, incl_s = ns;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int vf = __shfl_up(incl_f, off), vs = __shfl_up(incl_s, off);
+      if (lane >= off) { incl_f += vf; incl_s += vs; }
+    }
+    if (lane == 63) { P.wsum[0][wv] = incl_f; P.wsum[1][wv] = incl_s; }
+    // size classes of the short last splits: counts per (chunk, wave) and ranks inside the wave
+#pragma unroll
+    for (int k = 0; k < kPartBuckets; ++k) {
+      const unsigned long long m = __ballot(cls[c] == k);
+      if (lane == 0) P.cls_cnt[c][wv][k] = __popcll(m);
+      if (cls[c] == k) rank[c] = __popcll(m & ((1ull << lane) - 1ull));
+    }
+    __syncthreads();
+    int bf = carry_f, bs = carry_s, tf = 0, ts = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      if (w < wv) { bf += P.wsum[0][w]; bs += P.wsum[1][w]; }
+      tf += P.wsum[0][w];
+      ts += P.wsum[1][w];
+    }
+    if (b < B) { P.full_pre[b] = bf + incl_f - nf; P.split_pre[b] = bs + incl_s - ns; }
+    carry_f += tf;
+    carry_s += ts;
+    if (c + 1 < nch) __syncthreads();               // wsum is reused by the next chunk
+  }
+  if (wv == 0) {
+    // positions of the short splits: classes largest first, and inside a class (chunk, wave)
+    // order.  Lane l handles class l/4 and a quarter (4 consecutive (chunk, wave) entries) of it.
+    constexpr int E = C * kWaves;                   // (chunk, wave) entries per class
+    static_assert(E % 4 == 0, "quarters");
+    const int k = lane >> 2, q = lane & 3;
+    int cnt[E / 4], part = 0;
+#pragma unroll
+    for (int j = 0; j < E / 4; ++j) {
+      const int e = q * (E / 4) + j, c = e / kWaves, w = e - c * kWaves;
+      cnt[j] = c < nch ? P.cls_cnt[c][w][k] : 0;
+      part += cnt[j];
+    }
+    int incl = part;
+#pragma unroll
+    for (int off = 1; off < 4; off <<= 1) {
+      const int v = __shfl_up(incl, off, 4);
+      if (q >= off) incl += v;
+    }
+    const int total = __shfl(incl, (lane & ~3) + 3);   // the class's short splits
+    int t = q == 0 ? total : 0, cs = t;                 // inclusive scan of class totals over lanes
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int v = __shfl_up(cs, off);
+      if (lane >= off) cs += v;
+    }
+    int run = cs - total + incl - part;                  // class start + quarter start
+#pragma unroll
+    for (int j = 0; j < E / 4; ++j) {
+      const int e = q * (E / 4) + j, c = e / kWaves, w = e - c * kWaves;
+      P.cls_off[c][w][k] = run;
+      run += cnt[j];
+    }
+  }
+  if (tid == 0) {
+    P.full_pre[B] = carry_f;
+    P.split_pre[B] = carry_s;
+    P.n_full = carry_f;
+    P.err = err ? 1 : (carry_s > d.max_dec ? 2 : 0);
+    P.n_items = P.err ? 0 : carry_s * H;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int c = 0; c < C; ++c) {
+    const int b = c * kThreads + tid;
+    if (b < B && cls[c] >= 0) P.order[P.cls_off[c][wv][cls[c]] + rank[c]] = b;
+  }
+  __syncthreads();
+}
+
+// Work item `item` of the in-kernel plan: entries are the full splits in sequence order, then the
+// short last splits by size class; the kv-head runs fastest.
+__device__ __forceinline__ DecItem decode_item(const DecPlanLds& P, int item, int H, int B) {
+  const int e = item / H, g = item - e * H;
+  int b, split;
+  if (e < P.n_full) {
+    int lo = 0, hi = B - 1;                         // the last sequence whose full splits start at or before e
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (P.full_pre[mid] <= e) lo = mid; else hi = mid - 1;
+    }
+    b = lo;
+    split = e - P.full_pre[b];
+  } else {
+    b = P.order[e - P.n_full];
+    split = P.full_pre[b + 1] - P.full_pre[b];
+  }
+  return DecItem{b, split, g, b, P.kv[b], P.split_pre[b + 1] - P.split_pre[b], P.split_pre[b]};
+}
+
+template <int D>
+__global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a, DecPlanArgs d) {
+  constexpr int NW = kWaves;
+  // separate objects, so the LDS reads of one are known not to alias the LDS-DMA into the other
+  __shared__ __attribute__((aligned(16))) char vbufA[NW * VTile<D>::PAIR_BYTES];
+  __shared__ __attribute__((aligned(16))) char vbufB[NW * VTile<D>::PAIR_BYTES];
+  __shared__ DecPlanLds P;
+  __shared__ DecItem s_it[2];
+  __shared__ int s_flag;
+  int first = 0;
+  if (threadIdx.x == 0) first = atomicAdd(&a.ws_hdr[kHdrCounter], 1);   // in flight during the plan
+  decode_plan(a, d, P);
+  // the error flag shares a cache line with the work counter, so it is written only when set
+  // (then no work follows); the prologue cleared it
+  if (blockIdx.x == 0 && threadIdx.x == 0 && P.err) a.ws_hdr[kHdrError] = P.err;
+  const int n_items = P.n_items, pps = P.pps, H = a.num_kv_heads, B = d.batch;
+  const DecItem none{-1, 0, 0, 0, 0, 0, 0};
+  if (threadIdx.x == 0) s_it[0] = first < n_items ? decode_item(P, first, H, B) : none;
+  __syncthreads();
+  int slot = 0;
+  DecItem pend = none;                              // previous multi-split item, not yet counted in
+  while (s_it[slot].b >= 0) {
+    const DecItem it = s_it[slot];
+    int nx = 0;
+    if (threadIdx.x == 0) nx = atomicAdd(&a.ws_hdr[kHdrCounter], 1);   // used at the item's end
+    decode_split<D, NW, true>(a, it, pps, vbufA, vbufB, pend, &s_flag, [&] {
+      if (threadIdx.x == 0) s_it[slot ^ 1] = nx < n_items ? decode_item(P, nx, H, B) : none;
+    });                                             // ends with a barrier
+    slot ^= 1;
+  }
+  if (pend.b >= 0) {                                // the last item's count-in
+    __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
+    __syncthreads();
+    if (threadIdx.x == 0) s_flag = count_split_in(a, pend);
+    __syncthreads();
+    if (s_flag) merge_in_kernel<D, NW>(a, pend);
+  }
+}
+
+// Zeroes what the in-kernel decode plan needs zeroed: the workspace header (work counter, error
+// flag, the zero block) and the split counters.  A kernel, not a memset, so it can be captured.
+__global__ __launch_bounds__(256) void decode_prologue_kernel(int32_t* hdr, int32_t* split_cnt, int n_cnt) {
+  for (int i = threadIdx.x; i < n_cnt; i += 256) split_cnt[i] = 0;
+  if (threadIdx.x < kHdrWords) hdr[threadIdx.x] = 0;
 }
 
 // ------------------------------------------------------------------------------------------------
@@ -1228,6 +1655,7 @@ struct DevCache {
   std::atomic<int> ready{0};
   int num_cu = 0;
   int occ[2][4] = {{0, 0, 0, 0}, {0, 0, 0, 0}};   // [D == 128][kinds]
+  int occ_dec[2] = {0, 0};                        // decode_kernel, [D == 128]
   void* scratch = nullptr;                        // device address of this device's scratch array
   hipError_t scratch_err = hipSuccess;
 };
@@ -1239,12 +1667,20 @@ int occupancy_of() {
   return o;
 }
 
+template <int D>
+int occupancy_of_dec() {
+  int o = 1;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&o, decode_kernel<D>, kThreads, 0) != hipSuccess || o < 1) o = 1;
+  return o;
+}
+
 void fill_cache(DevCache& c, int dev) {
   hipDeviceProp_t prop;
   int ncu = 256;
   if (hipGetDeviceProperties(&prop, dev) == hipSuccess && prop.multiProcessorCount > 0) ncu = prop.multiProcessorCount;
   c.occ[0][1] = occupancy_of<64, 1>(); c.occ[0][2] = occupancy_of<64, 2>(); c.occ[0][3] = occupancy_of<64, 3>();
   c.occ[1][1] = occupancy_of<128, 1>(); c.occ[1][2] = occupancy_of<128, 2>(); c.occ[1][3] = occupancy_of<128, 3>();
+  c.occ_dec[0] = occupancy_of_dec<64>(); c.occ_dec[1] = occupancy_of_dec<128>();
   c.num_cu = ncu;
   void* p = nullptr;
   c.scratch_err = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
@@ -1316,6 +1752,25 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t 
     else if (kinds == 2) hipLaunchKernelGGL((attn_kernel<128, 2>), g, dim3(KernelCfg<128, 2>::NT), 0, stream, a, max_pre);
     else hipLaunchKernelGGL((attn_kernel<128, 3>), g, dim3(KernelCfg<128, 3>::NT), 0, stream, a, max_pre);
   }
+  return hipGetLastError();
+}
+
+hipError_t launch_decode_prologue(const AttnArgs& a, int batch, hipStream_t stream) {
+  hipLaunchKernelGGL(decode_prologue_kernel, dim3(1), dim3(256), 0, stream, a.ws_hdr, a.split_cnt,
+                     batch * a.num_kv_heads);
+  return hipGetLastError();
+}
+
+hipError_t launch_decode(const AttnArgs& a, const DecPlanArgs& d, int head_dim, int64_t max_items,
+                         hipStream_t stream) {
+  if (max_items <= 0) return hipSuccess;
+  const DevCache& c = dev_cache();
+  int64_t grid = (int64_t)c.num_cu * c.occ_dec[head_dim == 128 ? 1 : 0];
+  if (grid > max_items) grid = max_items;
+  if (head_dim == 64)
+    hipLaunchKernelGGL(decode_kernel<64>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, d);
+  else
+    hipLaunchKernelGGL(decode_kernel<128>, dim3((unsigned)grid), dim3(kThreads), 0, stream, a, d);
   return hipGetLastError();
 }
 

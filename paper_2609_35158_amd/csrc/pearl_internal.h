@@ -37,6 +37,10 @@ constexpr int kMaxPreSplitItems = 2 * kPlanComputeUnits;
 constexpr int kMaxQLen = 1 << 21;        // tiles per sequence < 2^16 (>= 32 tokens per tile)
 constexpr int kMaxKvLen = 1 << 25;       // splits per tile < 2^15 (>= 1024 keys per split)
 
+// Decode batches of up to this many sequences are planned inside the attention kernel (in LDS);
+// larger ones go through plan_kernel.
+constexpr int kDecPlanMaxSeqs = 1024;
+
 enum Mode : int { kModePrefill = 0, kModeDecode = 1, kModeMixed = 2 };
 
 // Kinds recorded per sequence by the planner.
@@ -68,7 +72,7 @@ struct SeqInfo {
 
 // Offsets (bytes) of the workspace regions; all 256-byte aligned.
 struct WsLayout {
-  size_t hdr, seqinfo, split_base, entries, part_o, part_ml, pre_jobs, part_pre_o, part_pre_ml, total;
+  size_t hdr, seqinfo, split_base, entries, part_o, part_ml, pre_jobs, part_pre_o, part_pre_ml, split_cnt, total;
   int64_t max_pre, max_dec;
   int64_t pre_slots;     // partial slots for split prefill items (0: prefill tiles never split)
   int64_t pre_jobs_cap;  // capacity of the prefill merge-job list
@@ -108,6 +112,13 @@ struct AttnArgs {
   const int4* pre_jobs;      // (sequence, tile, first entry, splits) per split prefill tile
   float* part_pre_o;         // [slot][kRowsPerTile][D] unnormalised partial outputs
   float* part_pre_ml;        // [slot][kRowsPerTile][2] running max (log2 units) and sum
+  int32_t* split_cnt;        // [batch][num_kv_heads] splits finished per pair (decode planned in-kernel)
+  // fused append and decode (decode planned in-kernel only): the new token's K/V rows
+  // [batch][num_kv_heads][D], or null; the pools again, writable
+  const uint16_t* k_new;
+  const uint16_t* v_new;
+  uint16_t* k_pool_w;
+  uint16_t* v_pool_w;
   int bt_stride;
   int num_pages;
   int num_q_heads;
@@ -115,6 +126,15 @@ struct AttnArgs {
   int group;
   int tokens_per_tile;
   float scale_log2;          // softmax_scale * log2(e)
+};
+
+// Arguments of the in-kernel decode plan.
+struct DecPlanArgs {
+  const int32_t* ctx_lens;
+  int batch;
+  int max_kv_len;
+  int pps_min;           // least pages per split (the host's bound, which sizes the workspace)
+  int max_dec;           // partial slots in the workspace
 };
 
 WsLayout workspace_layout(int batch, int total_q, int max_kv_len, int num_q_heads,
@@ -150,6 +170,11 @@ hipError_t launch_attention(const AttnArgs& a, int head_dim, int kinds, int64_t 
                             hipStream_t stream);
 
 hipError_t launch_merge(const AttnArgs& a, int head_dim, int batch, hipStream_t stream);
+
+// Decode planned in-kernel (batch <= kDecPlanMaxSeqs): the zeroing prologue, then the kernel.
+hipError_t launch_decode_prologue(const AttnArgs& a, int batch, hipStream_t stream);
+hipError_t launch_decode(const AttnArgs& a, const DecPlanArgs& d, int head_dim, int64_t max_items,
+                         hipStream_t stream);
 
 // Merge of split prefill tiles; jobs_cap bounds the device-side job count.
 hipError_t launch_merge_prefill(const AttnArgs& a, int head_dim, int64_t jobs_cap, hipStream_t stream);

@@ -181,3 +181,21 @@ def test_decode_static_host_validation():
     assert ws_bytes(shape(), big) > lib.pearl_attn_decode_static_max_bytes()
     st, msg = call_static(shape(), big)
     assert st == UNSUPPORTED and "static limit" in msg
+
+
+def test_decode_append_host_validation():
+    """The fused append-and-decode checks k_new / v_new and the decode layout before any HIP call."""
+    lib = pa.load()
+
+    def fused(s, d, k_new=FAKE, v_new=FAKE, ws=FAKE, wsb=1 << 30):
+        st = lib.pearl_attn_decode_append(ctypes.byref(s), ctypes.byref(d), FAKE, k_new, v_new, FAKE, FAKE, 0.1,
+                                          FAKE, None, ws, wsb, None)
+        return st, pa.last_error()
+
+    assert fused(shape(), desc(), k_new=None)[0] == INVALID
+    assert fused(shape(), desc(), v_new=None)[0] == INVALID
+    assert fused(shape(), desc(), k_new=FAKE + 8)[0] == INVALID
+    st, msg = fused(shape(), desc(cu=FAKE))
+    assert st == INVALID and "cu_q_lens" in msg
+    assert fused(shape(hq=32, hkv=2), desc())[0] == UNSUPPORTED
+    assert fused(shape(), desc(), wsb=16)[0] == WORKSPACE

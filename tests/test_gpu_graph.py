@@ -1,6 +1,6 @@
-"""The decode step (kv_append + decode attention) needs no host synchronisation or allocation, so
-it can be captured once in a HIP graph and replayed (the paper notes graph recapture as part of
-a reconfiguration's cost; section 4.3.2).  Each replay, with eager work and synchronisations in
+"""The decode step (kv_append + decode attention, or the two fused in pearl_attn_decode_append)
+needs no host synchronisation or allocation, so it can be captured once in a HIP graph and
+replayed (the paper notes graph recapture as part of a reconfiguration's cost; section 4.3.2).  Each replay, with eager work and synchronisations in
 between, must equal the eager call bit for bit and the oracle within tolerance."""
 import numpy as np
 import pytest
@@ -18,8 +18,9 @@ def _bf16(shape, gen):
     return torch.randn(shape, generator=gen, device="cuda", dtype=torch.float32).to(torch.bfloat16)
 
 
-def test_decode_step_graph_replays_match_eager():
-    say("case: decode step captured in a graph, 3 replays")
+@pytest.mark.parametrize("fused", [False, True], ids=["append+decode", "decode_append"])
+def test_decode_step_graph_replays_match_eager(fused):
+    say("case: decode step (%s) captured in a graph, 3 replays" % ("decode_append" if fused else "append + decode"))
     rng = np.random.default_rng(61)
     ctx = rng.integers(500, 4000, size=6, endpoint=True)
     case = workloads.build_case("graph", 6100, 8, 2, 128, ctx, np.ones(6, np.int64), device="cuda")
@@ -36,6 +37,10 @@ def test_decode_step_graph_replays_match_eager():
     ws_e = torch.empty_like(ws_g)
 
     def step(q, k, v, out, lse, ws):
+        if fused:
+            pa.decode_append(q, k, v, case.k_pool, case.v_pool, case.block_table, ctx_d, max_kv, scale=case.scale,
+                             out=out, lse=lse, workspace=ws)
+            return
         pa.kv_append(k, v, case.k_pool, case.v_pool, case.block_table, ctx_d, None, 1, max_kv)
         pa.decode(q, case.k_pool, case.v_pool, case.block_table, ctx_d, max_kv, scale=case.scale,
                   out=out, lse=lse, workspace=ws)

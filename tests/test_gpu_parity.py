@@ -383,20 +383,23 @@ def test_prefill_key_splits_long_context_sampled():
 
 
 def test_batches_larger_than_one_planner_chunk():
-    """More sequences than the planner's 256 threads: the block scans carry offsets from one
-    chunk of sequences to the next (decode: 1500 sequences; mixed: 1100 sequences with ragged
-    chunks and decodes; decode: 300 sequences long enough for several full splits each, so the
-    full splits, the short last splits and their size classes all span chunks)."""
-    say("case: 300-sequence decode with multi-split sequences")
+    """More sequences than one pass of the planners' threads: the block scans carry offsets from
+    one chunk of sequences to the next.  Decode of 800 sequences long enough for several full
+    splits each is planned inside the attention kernel (512 sequences per chunk), so its full
+    splits, short last splits and their size classes span chunks; decode of 1500 sequences (above
+    the in-kernel limit) and a mixed batch of 1100 sequences with ragged chunks go through the
+    planner kernel (256 sequences per chunk)."""
+    say("case: 800-sequence decode with multi-split sequences")
     rng = np.random.default_rng(78)
-    ctx = rng.integers(0, 3000, size=300, endpoint=True)
+    ctx = rng.integers(0, 3000, size=800, endpoint=True)
     ctx[:5] = (16 * 64, 16 * 64 - 1, 16 * 128, 0, 1)      # split-size multiples and edges
-    case = workloads.build_case("big-batch-splits", 7703, 8, 2, 64, ctx, np.ones(300, np.int64), device="cuda")
+    ctx[600:605] = (16 * 160 - 1, 16 * 160, 0, 2999, 1)  # and in the second chunk
+    case = workloads.build_case("big-batch-splits", 7703, 8, 2, 64, ctx, np.ones(800, np.int64), device="cuda")
     kr, vr = _append_and_check(case)
     o_ref, l_ref = oracle_full(case, kr, vr)
     out, lse = gpu_attend(case, "decode")
     torch.cuda.synchronize()
-    assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="300-sequence multi-split decode")
+    assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="800-sequence multi-split decode")
     say("case: 1500-sequence decode and 1100-sequence mixed batch")
     rng = np.random.default_rng(77)
     ctx = rng.integers(0, 90, size=1500, endpoint=True)
