@@ -30,6 +30,7 @@
 #include <math.h>
 
 #include <atomic>
+#include <type_traits>
 #include <mutex>
 
 namespace pearl {
@@ -450,19 +451,21 @@ __device__ __forceinline__ void lds_dma16_untracked(const void* g, const char* l
 
 // vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
 #define PEARL_VMCNT(n) (((n) & 15) | (((n) >> 4) << 14) | 0x0F70)
+// lgkmcnt(0) with the other counters left alone
+#define PEARL_LGKMCNT0 0xC07F
 
 // A prefill stage staged by LDS-DMA: kKeysPerStage key rows of D bf16, unpadded.  The 16-byte
 // chunk q of row r sits in slot q ^ swz(r), which keeps both operand read patterns free of bank
 // conflicts: the row reads of the Q.K products (16 consecutive rows, one chunk) and the
 // transposing reads of the P.V products (4 consecutive rows x 2 adjacent chunks).  Wave w copies
 // rows [RPW w, RPW w + RPW) of the stage, RPI rows per 64-lane DMA instruction.
-template <int D> struct DmaTile {
+template <int D, int KEYS = kKeysPerStage> struct DmaTile {
   static_assert(D == 64 || D == 128, "head_dim");
   static constexpr int CPR = D / 8;                 // 16-byte chunks per row
   static constexpr int RB = D * 2;                  // bytes per row
-  static constexpr int BYTES = kKeysPerStage * RB;
+  static constexpr int BYTES = KEYS * RB;
   static constexpr int RPI = 64 / CPR;              // rows per DMA instruction
-  static constexpr int RPW = kKeysPerStage / kWaves;   // rows copied per wave
+  static constexpr int RPW = KEYS / kWaves;         // rows copied per wave
   static constexpr int NDMA = RPW / RPI;            // DMA instructions per wave and tensor
   static_assert(NDMA >= 1 && NDMA * RPI == RPW && kPage % RPW == 0, "DMA split");
   __device__ static __forceinline__ int swz(int r) {
@@ -758,6 +761,356 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
 }
 
 // ------------------------------------------------------------------------------------------------
+// Prefill-append work item for the prefill-only kernel, with the matrix and vector work of the two
+// waves on each SIMD overlapped.  Same item, tile, operand layouts and softmax as prefill_tile; the
+// difference is the schedule.  The 8 waves form two groups, waves 0-3 and waves 4-7 (the waves
+// w and w + 4 share a SIMD), and the item runs in phases separated by workgroup barriers.  In each
+// of its phases a wave does either
+//   M(j): S(j) = K(j) Q^T and O += V(j-1)^T P(j-1)   (32 MFMAs at d = 128, no dependence between
+//         the two products), or
+//   V(j): the online softmax of S(j), giving P(j)    (exp, scale and sums on the vector ALU),
+// alternating M(0) V(0) M(1) V(1) ... M(n); group B runs one phase behind group A.  In every phase
+// one wave of each SIMD therefore issues MFMAs while the other runs its softmax, so the matrix core
+// works through the vector phase of the other wave instead of waiting for it.
+// Stages travel by LDS-DMA as before: K(j) into K buffer j % 3, V(j) into V buffer j % 3.  K(j) is
+// read in phases 2j and 2j+1, V(j) in phases 2j+2 and 2j+3; phase 2j issues the copies of K(j+2)
+// and V(j+1), each into a buffer whose last reader finished before the phase began.  Before phase
+// 2j every wave waits for its own copies of K(j) and V(j-1) (the copies issued since stay in
+// flight), and the barrier makes every wave's copies visible.
+// ------------------------------------------------------------------------------------------------
+template <int D>
+__device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
+                                                char* kb0, char* vb0) {
+  constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
+  constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
+  constexpr int SK = kKeysPerStage;                 // keys per stage
+  constexpr int NST = SK / 32;                      // 32-key sub-tiles per stage
+  static_assert(kKeysPerStage % SK == 0, "key splits stay stage-aligned");
+  using DT = DmaTile<D, SK>;
+  constexpr int RB = DT::RB;
+  // buffer r of each tensor (r = stage % 3 is a compile-time constant wherever a buffer is used, so
+  // every LDS address is a per-lane offset plus an immediate)
+  auto kbuf = [&](int r) { return kb0 + r * DT::BYTES; };
+  auto vbuf = [&](int r) { return vb0 + r * DT::BYTES; };
+
+  const int lane = threadIdx.x & 63, half = lane >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
+  const int grp = w >> 2;                           // 0: waves 0-3, 1: waves 4-7 (one phase later)
+  const SeqInfo si = a.seqinfo[b];
+  const int G = a.group;
+  const int tile = code & 0xffff, split = code >> 16;
+  const int t0 = tile * a.tokens_per_tile;
+  const int t_end = min(t0 + a.tokens_per_tile, si.q_len);
+  const int ctx = si.ctx_len;
+  const int kv_needed = ctx + t_end;
+  const int rho = 32 * w + (lane & 31);
+  const int tok = t0 + rho / G;
+  const int hh = rho - (rho / G) * G;
+  const int h = g * G + hh;
+  const bool row_ok = tok < t_end;
+  const int row_limit = ctx + tok;                  // last visible key of this row
+  const int wave_min_limit = ctx + t0 + (32 * w) / G;
+  const int H_q = a.num_q_heads, H_kv = a.num_kv_heads;
+  const size_t head_stride = (size_t)kPage * D;     // elements per (page, kv-head) block
+  const float c = a.scale_log2;
+
+  bf16x8 qop[KB];
+  {
+    const uint16_t* qrow = a.q + ((size_t)(si.q_start + (row_ok ? tok : t0)) * H_q + h) * D + 8 * half;
+#pragma unroll
+    for (int kb = 0; kb < KB; ++kb) qop[kb] = row_ok ? as_bf16x8(ld16(qrow + 16 * kb)) : zero_bf16x8();
+  }
+  f32x16 oacc[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[mb][r] = 0.f;
+  float m_run = -INFINITY, l_run = 0.f;
+
+  const int n_steps = (kv_needed + SK - 1) / SK;
+  const int n_split = tile_splits(ctx, t0, split_keys);
+  const int step_begin = split * (split_keys / SK);
+  const int step_end = split + 1 < n_split ? step_begin + split_keys / SK : n_steps;
+  const int n = step_end - step_begin;              // stages of this item (>= 1)
+
+  const ConstI32Ptr bt_c = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
+  const int last_pidx = (kv_needed - 1) / kPage;
+  const int gi = lane >> 4, jl = lane & 15;
+  const int krow = 4 * (gi >> 1) + (jl >> 2);
+  const int dcol = 16 * (gi & 1) + 4 * (jl & 3);
+  int koff[KB], voff[2][MB], goff[DT::NDMA];
+#pragma unroll
+  for (int kb = 0; kb < KB; ++kb) koff[kb] = (lane & 31) * RB + (((2 * kb + half) ^ DT::swz(lane & 15)) << 4);
+#pragma unroll
+  for (int sec = 0; sec < 2; ++sec)
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb) {
+      const int r = krow + 8 * sec;
+      voff[sec][mb] = r * RB + ((((32 * mb + dcol) >> 3) ^ DT::swz(r)) << 4) + (jl & 1) * 8;
+    }
+#pragma unroll
+  for (int i = 0; i < DT::NDMA; ++i) {
+    const int r = DT::RPW * w + DT::RPI * i + lane / DT::CPR;
+    goff[i] = (r % kPage) * RB + (((lane % DT::CPR) ^ DT::swz(r)) << 4);
+  }
+  // this wave's rows of the K (or V) tile of local stage j, by LDS-DMA; V rows past the last
+  // needed key come from the workspace's zero block (K rows there are always masked)
+  const char* zero_src = reinterpret_cast<const char*>(a.ws_hdr + kHdrZero);
+  // page id of this wave's rows of local stage j (scalar; read a phase pair before it is used)
+  auto page_of = [&](int j) {
+    const int pidx = min(((step_begin + j) * SK + DT::RPW * w) / kPage, last_pidx);
+    return clamp_page(bt_c[pidx], a.num_pages);
+  };
+  auto dma = [&](int j, bool is_v, int page, char* dst) {
+    const int step = step_begin + j;
+    const size_t base = (((size_t)page * H_kv + g) * head_stride) * 2;
+    const char* src = reinterpret_cast<const char*>(is_v ? a.v_pool : a.k_pool) + base;
+#pragma unroll
+    for (int i = 0; i < DT::NDMA; ++i) {
+      const int key = step * SK + DT::RPW * w + DT::RPI * i + lane / DT::CPR;
+      const int row0 = DT::RPW * w + DT::RPI * i;
+      lds_dma16_untracked(is_v && key >= kv_needed ? zero_src : src + goff[i], dst + row0 * RB);
+    }
+  };
+
+  f32x16 s[NST];                                    // S^T of the stage between its M and V phases
+  bf16x8 pop[NST][2];                               // P^T of the stage between its V and next M phases
+  const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int st = 0; st < NST; ++st) s[st] = zero16;
+#pragma unroll
+  for (int st = 0; st < NST; ++st)
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) pop[st][kk] = zero_bf16x8();
+
+  // M(j): PV of stage j - 1 (if any), then QK of stage j (if any).  P(j - 1) dies before S(j) is
+  // born, so the two share registers.  The phase is one wave's stream of MFMAs while the other
+  // wave of its SIMD runs a softmax, so nothing else hides its LDS latency: the operands are read
+  // kLead MFMAs ahead through a small ring, and a scheduling barrier after each step keeps that
+  // order (the compiler would otherwise read each operand just before its MFMA).
+  constexpr int NPV = 2 * NST * MB, NQK = NST * KB, kLead = 3;
+  auto operand = [&](int i, const char* kb_, const char* vb_) -> bf16x8 {
+    if (i < NPV) {                                  // V^T of (dim block, sub-tile, 16-key half)
+      const int mb = i / (2 * NST), st = (i >> 1) % NST, kk = i & 1;
+      const int vo = (32 * st + 16 * kk) * RB;
+      return concat_tr(lds_read_tr(vb_, vo + voff[0][mb]), lds_read_tr(vb_, vo + voff[1][mb]));
+    }
+    const int q = i - NPV, st = q / KB, kb = q - (q / KB) * KB;   // K rows of (sub-tile, k block)
+    return *reinterpret_cast<const bf16x8*>(kb_ + 32 * st * RB + koff[kb]);
+  };
+  auto mfma_slot = [&](int i, const bf16x8& op) {
+    if (i < NPV) {
+      const int mb = i / (2 * NST), st = (i >> 1) % NST, kk = i & 1;
+      oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op, pop[st][kk], oacc[mb], 0, 0, 0);
+    } else {
+      const int q = i - NPV, st = q / KB, kb = q - (q / KB) * KB;
+      s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
+    }
+  };
+  auto m_stream = [&](auto first_c, auto last_c, const char* kb_, const char* vb_) {
+    constexpr int first = decltype(first_c)::value, last = decltype(last_c)::value;
+    bf16x8 ring[kLead];
+#pragma unroll
+    for (int d = 0; d < kLead; ++d)
+      if (first + d < last) ring[d] = operand(first + d, kb_, vb_);
+#pragma unroll
+    for (int i = first; i < last; ++i) {
+      const bf16x8 op = ring[(i - first) % kLead];
+      if (i + kLead < last) ring[(i - first) % kLead] = operand(i + kLead, kb_, vb_);
+      mfma_slot(i, op);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // One instruction stream for every M phase (no joins of differently allocated copies): M(0)
+  // adds P = 0 times a zero-filled V buffer 2, and M(n) computes an S that no V phase reads.
+  // R = j % 3: K(j) sits in K buffer R and V(j - 1) in V buffer (R + 2) % 3.
+  auto phase_m = [&](auto r_c) {
+    constexpr int R = decltype(r_c)::value;
+    m_stream(std::integral_constant<int, 0>{}, std::integral_constant<int, NPV + NQK>{}, kbuf(R),
+             vbuf((R + 2) % 3));
+  };
+  // V(j), 0 <= j < n: causal mask (stages reaching past some row's last key), then the online
+  // softmax with a lagging maximum, exactly as in prefill_tile
+  auto phase_v = [&](int j) {
+    const int k0 = (step_begin + j) * SK;
+    if (k0 + SK - 1 > wave_min_limit) {
+      __asm__ volatile("" ::);
+#pragma unroll
+      for (int st = 0; st < NST; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int key = k0 + 32 * st + (r & 3) + 8 * (r >> 2) + 4 * half;
+          if (key > row_limit) s[st][r] = -INFINITY;
+        }
+    }
+    float ps0 = 0.f, ps1 = 0.f;
+#pragma unroll
+    for (int st = 0; st < NST; ++st)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_run));
+        if (r & 1) ps1 += pv; else ps0 += pv;
+        pop[st][r >> 3][r & 7] = (__bf16)pv;
+      }
+    float psum = ps0 + ps1;
+    if (__ballot(!(psum <= kMaxWeightSum))) {
+      __asm__ volatile("" ::);
+      float mx = s[0][0];
+#pragma unroll
+      for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
+#pragma unroll
+      for (int st = 1; st < NST; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[st][r]);
+      mx = xor32_max(mx);
+      const bool grow = mx * c > m_run + kMaxLag;
+      const float m_new = grow ? mx * c : m_run;
+      const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
+      ps0 = ps1 = 0.f;
+#pragma unroll
+      for (int st = 0; st < NST; ++st)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
+          if (r & 1) ps1 += pv; else ps0 += pv;
+          pop[st][r >> 3][r & 7] = (__bf16)pv;
+        }
+      psum = ps0 + ps1;
+      l_run *= alpha;
+      if (__ballot(grow)) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
+      }
+      m_run = m_new;
+    }
+    l_run += psum;
+  };
+  // end of phase t: wait for this wave's copies that phase t + 1 reads (before an M phase of group
+  // A, K(j) and V(j - 1) of j = (t + 1) / 2, copied at phase 2j - 4; the copies of phase 2j - 2
+  // stay in flight), drain the LDS reads, and pass the barrier without the release fence of
+  // __syncthreads (which would drain every copy)
+  constexpr int P = DT::NDMA;                       // DMA instructions per tensor and stage
+  auto end_phase = [&](int t) {
+    if ((t & 1) != 0) {
+      const int j = (t + 1) >> 1;
+      const int later = (j + 1 < n) + (j < n);      // copies issued after V(j - 1): K(j + 1), V(j)
+      if (later == 2) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(2 * P));
+      else if (later == 1) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(P));
+      else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
+    }
+    __builtin_amdgcn_s_waitcnt(PEARL_LGKMCNT0);
+    __asm__ volatile("s_barrier" ::: "memory");
+  };
+
+  // prologue: K(0), V(0), K(1), and zeros into V buffer 2 (read by M(0), whose P is 0; V(2) is
+  // copied there only in phase 2); the first M phase needs K(0).  Even phase 2j copies K(j + 2)
+  // and V(j + 1), whose page ids were read at phase 2j - 2.
+  int pid_v = 1 < n ? page_of(1) : 0, pid_k = 2 < n ? page_of(2) : 0;
+  {
+    const int p0 = page_of(0);
+    dma(0, false, p0, kbuf(0));
+    dma(0, true, p0, vbuf(0));
+  }
+  if (1 < n) dma(1, false, pid_v, kbuf(1));
+#pragma unroll
+  for (int i = 0; i < DT::NDMA; ++i)
+    lds_dma16_untracked(zero_src, vbuf(2) + (DT::RPW * w + DT::RPI * i) * RB);
+  __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));       // Q loads and the first copies (also this item's)
+  __asm__ volatile("s_barrier" ::: "memory");
+  // copies of even phase 2j (R = j % 3): K(j + 2) into K buffer (R + 2) % 3, V(j + 1) into V
+  // buffer (R + 1) % 3
+  auto copies = [&](auto r_c, int j) {
+    constexpr int R = decltype(r_c)::value;
+    if (j + 2 < n) dma(j + 2, false, pid_k, kbuf((R + 2) % 3));
+    if (j + 1 < n) dma(j + 1, true, pid_v, vbuf((R + 1) % 3));
+    pid_v = pid_k;
+    if (j + 3 < n) pid_k = page_of(j + 3);
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  // Each group runs its own loop (the same barriers in the same number: 2n + 2), so the registers
+  // of S and P are never live together on any path.  The loops are unrolled over the three buffers
+  // and no phase is conditional inside them.
+  if (grp == 0) {
+    // phases 2j, 2j + 1 for j < n: M(j), V(j); then M(n) and an empty phase
+    auto step = [&](auto r_c, int j) {
+      copies(r_c, j);
+      phase_m(r_c);
+      end_phase(2 * j);
+      phase_v(j);
+      end_phase(2 * j + 1);
+    };
+    int j = 0;
+    for (; j + 3 <= n; j += 3) {
+      step(I0{}, j);
+      step(I1{}, j + 1);
+      step(I2{}, j + 2);
+    }
+    if (j < n) { step(I0{}, j); ++j; }
+    if (j < n) { step(I1{}, j); ++j; }
+    const int r = n % 3;                            // j == n
+    if (r == 0) phase_m(I0{}); else if (r == 1) phase_m(I1{}); else phase_m(I2{});
+    end_phase(2 * n);
+    end_phase(2 * n + 1);
+  } else {
+    // phases 0, 1: an empty phase, M(0); phases 2j, 2j + 1 for 1 <= j <= n: V(j - 1), M(j)
+    auto step = [&](auto r_c, int j) {
+      copies(r_c, j);
+      phase_v(j - 1);
+      end_phase(2 * j);
+      phase_m(r_c);
+      end_phase(2 * j + 1);
+    };
+    copies(I0{}, 0);
+    end_phase(0);
+    phase_m(I0{});
+    end_phase(1);
+    int j = 1;
+    for (; j + 3 <= n + 1; j += 3) {
+      step(I1{}, j);
+      step(I2{}, j + 1);
+      step(I0{}, j + 2);
+    }
+    if (j <= n) { step(I1{}, j); ++j; }
+    if (j <= n) { step(I2{}, j); ++j; }
+  }
+
+  // epilogue (as in prefill_tile): combine the half-row sums; a split item stores its partial state
+  const float l_tot = xor32_add(l_run);
+  if (row_ok && n_split > 1) {
+    const size_t prow = (size_t)(e * H_kv + g) * kRowsPerTile + rho;
+    float* po = a.part_pre_o + prow * D;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq)
+        *reinterpret_cast<f32x4*>(po + 32 * mb + 8 * rq + 4 * half) =
+            f32x4{oacc[mb][4 * rq + 0], oacc[mb][4 * rq + 1], oacc[mb][4 * rq + 2], oacc[mb][4 * rq + 3]};
+    if (half == 0) {
+      a.part_pre_ml[2 * prow] = m_run;
+      a.part_pre_ml[2 * prow + 1] = l_tot;
+    }
+  } else if (row_ok) {
+    const float inv = 1.0f / l_tot;
+    uint16_t* orow = a.out + ((size_t)(si.q_start + tok) * H_q + h) * D;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int rq = 0; rq < 4; ++rq) {
+        const int dim = 32 * mb + 8 * rq + 4 * half;
+        u32x2 pk;
+        pk[0] = (uint32_t)bf16_bits(oacc[mb][4 * rq + 0] * inv) | ((uint32_t)bf16_bits(oacc[mb][4 * rq + 1] * inv) << 16);
+        pk[1] = (uint32_t)bf16_bits(oacc[mb][4 * rq + 2] * inv) | ((uint32_t)bf16_bits(oacc[mb][4 * rq + 3] * inv) << 16);
+        *reinterpret_cast<u32x2*>(orow + dim) = pk;
+      }
+    if (half == 0 && a.lse) a.lse[(size_t)(si.q_start + tok) * H_q + h] = (m_run + flog2(l_tot)) * kLn2;
+  }
+}
+
+// ------------------------------------------------------------------------------------------------
 // Decode work item: one (sequence, kv-head g, split of pps pages; the planner chooses pps).  The
 // G q-heads of the group are the 16 columns of 16x16x32 MFMAs (columns >= G are zero), so each
 // K/V byte is loaded once for the whole group.  Wave w takes page pairs w, w+8, ... of the split:
@@ -1016,9 +1369,6 @@ __device__ __forceinline__ int count_split_in(const AttnArgs& a, const DecItem& 
   return prev == it.n_splits - 1;
 }
 
-// lgkmcnt(0) with the other counters left alone (gfx9 encoding)
-#define PEARL_LGKMCNT0 0xC07F
-
 // One pipeline step: issue the next pair (K into k_next, V by DMA into v_next), then consume the
 // current pair from k_cur / v_cur.  The step is branch-free: a wave with no further pair re-issues
 // its current pair (L2 hits, results unused), so every step leaves exactly one pair in flight.
@@ -1217,8 +1567,9 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   __shared__ __attribute__((aligned(16))) char vbufB_[(kKinds == 2) ? NW * VTile<D>::PAIR_BYTES : 16];
   char* vbufA = (kKinds == 2) ? vbufA_ : smem;
   char* vbufB = (kKinds == 2) ? vbufB_ : smem + NW * VTile<D>::PAIR_BYTES;
+  // prefill-only kernels: three K and three V stage buffers, each set contiguous
   constexpr int kDT = (kKinds == 1) ? DmaTile<D>::BYTES : 16;
-  __shared__ __attribute__((aligned(16))) char pk0[kDT], pk1[kDT], pk2[kDT], pv0[kDT], pv1[kDT], pv2[kDT];
+  __shared__ __attribute__((aligned(16))) char pk[3 * kDT], pv[3 * kDT];
   __shared__ int s_item[2];
   const int n_items = a.ws_hdr[kHdrNumItems];
   const int n_pre = a.ws_hdr[kHdrNumPre];
@@ -1262,7 +1613,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
         static_assert(NW == kWaves, "prefill tiles use 8 waves");
         const int2 en = a.entries[e];
         if constexpr (kKinds == 1) {
-          prefill_tile<D, true>(a, e, en.x, en.y, g, split_keys, pk0, pk1, pk2, pv0, pv1, pv2);
+          prefill_tile_pp<D>(a, e, en.x, en.y, g, split_keys, pk, pv);
         } else {
           // the mixed kernel's stage buffers share its LDS region with the decode V buffers (a
           // workgroup runs one item at a time, and items are separated by a drained barrier)
