@@ -456,9 +456,11 @@ __device__ __forceinline__ void lds_dma16_untracked(const void* g, const char* l
 
 // A prefill stage staged by LDS-DMA: kKeysPerStage key rows of D bf16, unpadded.  The 16-byte
 // chunk q of row r sits in slot q ^ swz(r), which keeps both operand read patterns free of bank
-// conflicts: the row reads of the Q.K products (16 consecutive rows, one chunk) and the
-// transposing reads of the P.V products (4 consecutive rows x 2 adjacent chunks).  Wave w copies
-// rows [RPW w, RPW w + RPW) of the stage, RPI rows per 64-lane DMA instruction.
+// conflicts on the 64 banks of 4 bytes: the row reads of the Q.K products (16 lanes read one chunk
+// of 16 consecutive rows: swz is a permutation of the 16 rows' slots) and the transposing reads of
+// the P.V products (32 lanes read 4 adjacent chunks of 4 consecutive rows: swz moves each of the 4
+// rows to its own quarter of the 256 bank bytes).  Wave w copies rows [RPW w, RPW w + RPW) of the
+// stage, RPI rows per 64-lane DMA instruction.
 template <int D, int KEYS = kKeysPerStage> struct DmaTile {
   static_assert(D == 64 || D == 128, "head_dim");
   static constexpr int CPR = D / 8;                 // 16-byte chunks per row
@@ -469,8 +471,10 @@ template <int D, int KEYS = kKeysPerStage> struct DmaTile {
   static constexpr int NDMA = RPW / RPI;            // DMA instructions per wave and tensor
   static_assert(NDMA >= 1 && NDMA * RPI == RPW && kPage % RPW == 0, "DMA split");
   __device__ static __forceinline__ int swz(int r) {
-    if constexpr (D == 128) return ((r & 3) << 1) | ((r >> 2) & 1) | (r & 8);
-    else return (((r >> 1) & 1) << 1) | ((r >> 2) & 1) | (((r >> 3) & 1) << 2);
+    // d = 128: a row is all 64 banks, rows 4i..4i+3 get slot offsets 0, 4, 8, 12 (+ i);
+    // d = 64: two rows share the banks, rows 4i..4i+3 get offsets 0, 0, 4, 4 (+ i)
+    if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+    else return (((r >> 1) & 1) << 2) | ((r >> 2) & 3);
   }
 };
 
