@@ -51,6 +51,9 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 __device__ __forceinline__ bf16x8 zero_bf16x8() { return as_bf16x8(u32x4{0u, 0u, 0u, 0u}); }
 
 __device__ __forceinline__ float fexp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// The XCD this wave runs on (hardware register XCC_ID, bits 3:0), in [0, kNumXcd).
+__device__ __forceinline__ int xcc_id() { return __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11)) % kNumXcd; }
 __device__ __forceinline__ float flog2(float x) { return __builtin_amdgcn_logf(x); }
 
 __device__ __forceinline__ uint16_t bf16_bits(float x) { return __builtin_bit_cast(uint16_t, (__bf16)x); }
@@ -174,6 +177,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
   if (tid < kPartBuckets) { s_part_cnt[tid] = 0; s_tile_cnt[tid] = 0; }
   if (tid < kHdrWords - kHdrZero) hdr[kHdrZero + tid] = 0;   // zero block read by decode items
+  if (tid < kNumXcd) hdr[kHdrQueues + tid] = 0;
   __syncthreads();
   // pass 1: validate every sequence and total the work
   // sequence tid's lengths (first chunk), kept for the later passes
@@ -777,10 +781,15 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
 // one wave of each SIMD therefore issues MFMAs while the other runs its softmax, so the matrix core
 // works through the vector phase of the other wave instead of waiting for it.
 // Stages travel by LDS-DMA as before: K(j) into K buffer j % 3, V(j) into V buffer j % 3.  K(j) is
-// read in phases 2j and 2j+1, V(j) in phases 2j+2 and 2j+3; phase 2j issues the copies of K(j+2)
-// and V(j+1), each into a buffer whose last reader finished before the phase began.  Before phase
-// 2j every wave waits for its own copies of K(j) and V(j-1) (the copies issued since stay in
-// flight), and the barrier makes every wave's copies visible.
+// read in phases 2j and 2j+1, V(j) in phases 2j+2 and 2j+3.  Each wave copies its rows of K(j+2)
+// and V(j+1) (the pair j) in phases 2j and 2j+1, into buffers last read in phase 2j-1: half of the
+// DMA instructions right after its MFMAs of M(j), the other half at the start of its adjacent
+// softmax phase.  A DMA instruction holds its wave for tens of cycles before it is accepted, and
+// longer when many queue at the compute unit at once: issued all together at a phase start they
+// stalled every wave for hundreds of cycles; after the MFMAs they overlap the draining matrix
+// pipeline, and at the start of a softmax phase they use the slack that phase has over an M phase.
+// Before the barrier that ends phase 2j-1 every wave waits for its own copies of K(j) and V(j-1)
+// (the copies issued since stay in flight).
 // ------------------------------------------------------------------------------------------------
 template <int D>
 __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
@@ -860,22 +869,29 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
   // this wave's rows of the K (or V) tile of local stage j, by LDS-DMA; V rows past the last
   // needed key come from the workspace's zero block (K rows there are always masked)
   const char* zero_src = reinterpret_cast<const char*>(a.ws_hdr + kHdrZero);
-  // page id of this wave's rows of local stage j (scalar; read a phase pair before it is used)
+  // block-table entry of this wave's rows of local stage j (a scalar load; clamped where used)
   auto page_of = [&](int j) {
     const int pidx = min(((step_begin + j) * SK + DT::RPW * w) / kPage, last_pidx);
-    return clamp_page(bt_c[pidx], a.num_pages);
+    return bt_c[pidx];
   };
-  auto dma = [&](int j, bool is_v, int page, char* dst) {
+  // DMA instruction i of this wave's rows of local stage j
+  auto dma_one = [&](int j, bool is_v, int entry, char* dst, int i) {
     const int step = step_begin + j;
+    const int page = clamp_page(entry, a.num_pages);
     const size_t base = (((size_t)page * H_kv + g) * head_stride) * 2;
     const char* src = reinterpret_cast<const char*>(is_v ? a.v_pool : a.k_pool) + base;
-#pragma unroll
-    for (int i = 0; i < DT::NDMA; ++i) {
-      const int key = step * SK + DT::RPW * w + DT::RPI * i + lane / DT::CPR;
-      const int row0 = DT::RPW * w + DT::RPI * i;
-      lds_dma16_untracked(is_v && key >= kv_needed ? zero_src : src + goff[i], dst + row0 * RB);
-    }
+    const int key = step * SK + DT::RPW * w + DT::RPI * i + lane / DT::CPR;
+    const int row0 = DT::RPW * w + DT::RPI * i;
+    lds_dma16_untracked(is_v && key >= kv_needed ? zero_src : src + goff[i], dst + row0 * RB);
   };
+  auto dma = [&](int j, bool is_v, int entry, char* dst) {
+#pragma unroll
+    for (int i = 0; i < DT::NDMA; ++i) dma_one(j, is_v, entry, dst, i);
+  };
+
+  // block-table entries of the next copies: pid_k for K rows, pid_v for V rows (pid_n: the K
+  // rows after those, read ahead by group B)
+  int pid_v = 1 < n ? page_of(1) : 0, pid_k = 2 < n ? page_of(2) : 0, pid_n = 0;
 
   f32x16 s[NST];                                    // S^T of the stage between its M and V phases
   bf16x8 pop[NST][2];                               // P^T of the stage between its V and next M phases
@@ -911,27 +927,38 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
       s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(op, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
     }
   };
-  auto m_stream = [&](auto first_c, auto last_c, const char* kb_, const char* vb_) {
-    constexpr int first = decltype(first_c)::value, last = decltype(last_c)::value;
-    bf16x8 ring[kLead];
-#pragma unroll
-    for (int d = 0; d < kLead; ++d)
-      if (first + d < last) ring[d] = operand(first + d, kb_, vb_);
-#pragma unroll
-    for (int i = first; i < last; ++i) {
-      const bf16x8 op = ring[(i - first) % kLead];
-      if (i + kLead < last) ring[(i - first) % kLead] = operand(i + kLead, kb_, vb_);
-      mfma_slot(i, op);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-  };
+  constexpr int NM = NPV + NQK;
   // One instruction stream for every M phase (no joins of differently allocated copies): M(0)
   // adds P = 0 times a zero-filled V buffer 2, and M(n) computes an S that no V phase reads.
   // R = j % 3: K(j) sits in K buffer R and V(j - 1) in V buffer (R + 2) % 3.
   auto phase_m = [&](auto r_c) {
     constexpr int R = decltype(r_c)::value;
-    m_stream(std::integral_constant<int, 0>{}, std::integral_constant<int, NPV + NQK>{}, kbuf(R),
-             vbuf((R + 2) % 3));
+    const char* kb_ = kbuf(R);
+    const char* vb_ = vbuf((R + 2) % 3);
+    bf16x8 ring[kLead];
+#pragma unroll
+    for (int d = 0; d < kLead; ++d) ring[d] = operand(d, kb_, vb_);
+#pragma unroll
+    for (int i = 0; i < NM; ++i) {
+      const bf16x8 op = ring[i % kLead];
+      if (i + kLead < NM) ring[i % kLead] = operand(i + kLead, kb_, vb_);
+      mfma_slot(i, op);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  };
+  // The copies of stage j's pair: K(j + 2) into K buffer (R + 2) % 3 and V(j + 1) into V buffer
+  // (R + 1) % 3 (R = j % 3).
+  auto copy_k = [&](auto r_c, int j) {
+    constexpr int R = decltype(r_c)::value;
+#pragma unroll
+    for (int i = 0; i < DT::NDMA; ++i)
+      if (j + 2 < n) dma_one(j + 2, false, pid_k, kbuf((R + 2) % 3), i);
+  };
+  auto copy_v = [&](auto r_c, int j) {
+    constexpr int R = decltype(r_c)::value;
+#pragma unroll
+    for (int i = 0; i < DT::NDMA; ++i)
+      if (j + 1 < n) dma_one(j + 1, true, pid_v, vbuf((R + 1) % 3), i);
   };
   // V(j), 0 <= j < n: causal mask (stages reaching past some row's last key), then the online
   // softmax with a lagging maximum, exactly as in prefill_tile
@@ -991,15 +1018,15 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     }
     l_run += psum;
   };
-  // end of phase t: wait for this wave's copies that phase t + 1 reads (before an M phase of group
-  // A, K(j) and V(j - 1) of j = (t + 1) / 2, copied at phase 2j - 4; the copies of phase 2j - 2
-  // stay in flight), drain the LDS reads, and pass the barrier without the release fence of
-  // __syncthreads (which would drain every copy)
+  // end of phase t: wait for this wave's copies that phase t + 1 reads (before M(j) of group A,
+  // j = (t + 1) / 2: K(j) and V(j - 1), the pair j - 2; those of the pair j - 1 stay in flight),
+  // drain the LDS reads, and pass the barrier without the release fence of __syncthreads (which
+  // would drain every copy)
   constexpr int P = DT::NDMA;                       // DMA instructions per tensor and stage
   auto end_phase = [&](int t) {
     if ((t & 1) != 0) {
       const int j = (t + 1) >> 1;
-      const int later = (j + 1 < n) + (j < n);      // copies issued after V(j - 1): K(j + 1), V(j)
+      const int later = (j + 1 < n) + (j < n);      // the pair j - 1: K(j + 1), V(j)
       if (later == 2) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(2 * P));
       else if (later == 1) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(P));
       else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
@@ -1009,9 +1036,11 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
   };
 
   // prologue: K(0), V(0), K(1), and zeros into V buffer 2 (read by M(0), whose P is 0; V(2) is
-  // copied there only in phase 2); the first M phase needs K(0).  Even phase 2j copies K(j + 2)
-  // and V(j + 1), whose page ids were read at phase 2j - 2.
-  int pid_v = 1 < n ? page_of(1) : 0, pid_k = 2 < n ? page_of(2) : 0;
+  // copied there only with the pair 1); the first M phase needs K(0).  Block-table entries are
+  // read in softmax phases, a phase or more before they are used: scalar loads share the LDS
+  // reads' counter and complete out of order, so one in flight during an M phase would make
+  // every operand wait drain the counter, and one used right away would stall the phase for a
+  // memory round trip.  The end-of-phase drain completes them.
   {
     const int p0 = page_of(0);
     dma(0, false, p0, kbuf(0));
@@ -1023,15 +1052,6 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     lds_dma16_untracked(zero_src, vbuf(2) + (DT::RPW * w + DT::RPI * i) * RB);
   __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));       // Q loads and the first copies (also this item's)
   __asm__ volatile("s_barrier" ::: "memory");
-  // copies of even phase 2j (R = j % 3): K(j + 2) into K buffer (R + 2) % 3, V(j + 1) into V
-  // buffer (R + 1) % 3
-  auto copies = [&](auto r_c, int j) {
-    constexpr int R = decltype(r_c)::value;
-    if (j + 2 < n) dma(j + 2, false, pid_k, kbuf((R + 2) % 3));
-    if (j + 1 < n) dma(j + 1, true, pid_v, vbuf((R + 1) % 3));
-    pid_v = pid_k;
-    if (j + 3 < n) pid_k = page_of(j + 3);
-  };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
   using I2 = std::integral_constant<int, 2>;
@@ -1039,11 +1059,16 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
   // of S and P are never live together on any path.  The loops are unrolled over the three buffers
   // and no phase is conditional inside them.
   if (grp == 0) {
-    // phases 2j, 2j + 1 for j < n: M(j), V(j); then M(n) and an empty phase
+    // phases 2j, 2j + 1 for j < n: M(j), V(j); then M(n) and an empty phase.  The K rows of the
+    // pair follow the MFMAs of M(j), the V rows open V(j), and the block-table entry of the next K
+    // rows is read during V(j).
     auto step = [&](auto r_c, int j) {
-      copies(r_c, j);
       phase_m(r_c);
+      copy_k(r_c, j);
       end_phase(2 * j);
+      copy_v(r_c, j);
+      pid_v = pid_k;
+      if (j + 3 < n) pid_k = page_of(j + 3);
       phase_v(j);
       end_phase(2 * j + 1);
     };
@@ -1060,17 +1085,29 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     end_phase(2 * n);
     end_phase(2 * n + 1);
   } else {
-    // phases 0, 1: an empty phase, M(0); phases 2j, 2j + 1 for 1 <= j <= n: V(j - 1), M(j)
+    // phases 0, 1: an empty phase, M(0); phases 2j, 2j + 1 for 1 <= j <= n: V(j - 1), M(j).  The
+    // K rows of pair j open V(j - 1) (phase 0 for pair 0), the V rows follow the MFMAs of M(j),
+    // and the block-table entry of the K rows after them is read during V(j - 1).
+    auto pair_done = [&]() {
+      pid_v = pid_k;
+      pid_k = pid_n;
+    };
     auto step = [&](auto r_c, int j) {
-      copies(r_c, j);
+      copy_k(r_c, j);
+      if (j + 3 < n) pid_n = page_of(j + 3);
       phase_v(j - 1);
       end_phase(2 * j);
       phase_m(r_c);
+      copy_v(r_c, j);
+      pair_done();
       end_phase(2 * j + 1);
     };
-    copies(I0{}, 0);
+    copy_k(I0{}, 0);
+    if (3 < n) pid_n = page_of(3);
     end_phase(0);
     phase_m(I0{});
+    copy_v(I0{}, 0);
+    pair_done();
     end_phase(1);
     int j = 1;
     for (; j + 3 <= n + 1; j += 3) {
@@ -1586,8 +1623,24 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   // each takes the other kind once its own is exhausted, so both kinds run side by side.
   const int n_pre_items = n_pre * H_kv;
   const bool pre_first = (int)blockIdx.x < a.ws_hdr[kHdrPreFirstWG];
+  // Prefill-only launches: item i belongs to queue i % 8, and a workgroup takes the items of the
+  // queue of the XCD it runs on, then those of the other queues in turn.  With 8 kv-heads (or a
+  // multiple or divisor of 8) the items of one (sequence, kv-head) then share one XCD's L2: every
+  // tile of a sequence re-reads that head's whole context, which other XCDs would each fetch
+  // from memory again.  The queues are balanced (the 8 heads of a tile are equal work), and the
+  // turn to other queues completes every item wherever the workgroups run.
+  int queue = xcc_id(), queues_left = kNumXcd;      // thread 0's claim state
   auto claim = [&]() -> int {
-    if constexpr (kKinds != 3) {
+    if constexpr (kKinds == 1) {
+      while (queues_left > 0) {
+        const int c = atomicAdd(&a.ws_hdr[kHdrQueues + queue], 1);
+        const int64_t i = queue + (int64_t)kNumXcd * c;
+        if (i < n_items) return (int)i;
+        queue = (queue + 1) % kNumXcd;
+        --queues_left;
+      }
+      return n_items;
+    } else if constexpr (kKinds == 2) {
       return atomicAdd(&a.ws_hdr[kHdrCounter], 1);
     } else {
       const int n_dec_items = n_items - n_pre_items;

@@ -37,6 +37,9 @@ constexpr int kMaxPreSplitItems = 2 * kPlanComputeUnits;
 constexpr int kMaxQLen = 1 << 21;        // tiles per sequence < 2^16 (>= 32 tokens per tile)
 constexpr int kMaxKvLen = 1 << 25;       // splits per tile < 2^15 (>= 1024 keys per split)
 
+// XCDs (accelerator complex dies) of an MI355X, each with its own L2.
+constexpr int kNumXcd = 8;
+
 // Decode batches of up to this many sequences are planned inside the attention kernel (in LDS);
 // larger ones go through plan_kernel.
 constexpr int kDecPlanMaxSeqs = 1024;
@@ -58,6 +61,7 @@ enum Hdr : int {
   kHdrCounterPre = 7,  // prefill work counter of mixed launches (atomic)
   kHdrPreFirstWG = 8,  // mixed launches: workgroups [0, this) take prefill items first
   kHdrPagesPerSplit = 9,  // pages per decode split chosen by the planner
+  kHdrQueues = 16,     // words 16..23: prefill-only launches, one work counter per XCD (atomic)
   kHdrZero = 32,       // words 32..63: a zeroed 128-byte block (source for keys past the end)
   kHdrWords = 64
 };
