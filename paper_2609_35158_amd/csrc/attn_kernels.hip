@@ -510,8 +510,13 @@ __device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, in
   auto kbuf = [&](int buf) { return kHoistV ? (buf == 0 ? kb0 : (buf == 1 ? kb1 : kb2)) : kb0 + buf * DT::BYTES; };
   auto vbuf = [&](int buf) { return kHoistV ? (buf == 0 ? vb0 : (buf == 1 ? vb1 : vb2)) : vb0 + buf * DT::BYTES; };
 
-  const int lane = threadIdx.x & 63, half = lane >> 5;
-  const int w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
+  // the thread index passes through an empty asm, so the per-lane offsets derived from it are
+  // computed per item: hoisted out of the mixed kernel's item loop, they stayed live across the
+  // decode items too and pushed that kernel past its registers
+  int tid = threadIdx.x;
+  __asm__ volatile("" : "+v"(tid));
+  const int lane = tid & 63, half = lane >> 5;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
   const SeqInfo si = a.seqinfo[b];
   const int G = a.group;
   const int tile = code & 0xffff, split = code >> 16;
