@@ -117,10 +117,13 @@ class EventPairs:
 
 
 def run_timed(torch, pa, step, steps, warmup, flush=None):
-    """Run `warmup` untimed steps, then `steps` timed steps bracketed by synchronize.  `step(hook)`
-    performs one step and calls hook() right before the library call whose kernel is timed.
-    With `flush` (a callable enqueuing the cache flush) every step is preceded by a flush, which
-    the kernel events do not include (the wall-clock step time then does).
+    """Run `warmup` untimed steps, then `steps` timed steps bracketed by synchronize (the wall-clock
+    step time), then `steps` more with HIP events around the timed kernel of each step (the
+    kernel times).  The events are recorded into the stream between the kernels of a step and
+    hold the next kernel back by a few microseconds, so the step time comes from the run without
+    them.  `step(hook)` performs one step and calls hook() right before the library call whose
+    kernel is timed.  With `flush` (a callable enqueuing the cache flush) every step is preceded
+    by a flush, which the kernel events do not include (the wall-clock step time then does).
     Returns (wall ms per step, mean kernel ms, per-launch kernel ms)."""
     pairs = EventPairs(torch, steps)
     for _ in range(warmup):
@@ -129,13 +132,18 @@ def run_timed(torch, pa, step, steps, warmup, flush=None):
         step(lambda: None)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
+    for _ in range(steps):
+        if flush:
+            flush()
+        step(lambda: None)
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
     for i in range(steps):
         if flush:
             flush()
         h = pairs.handles(i)
         step(lambda h=h: pa.binding.set_kernel_events(*h))
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
     pa.binding.set_kernel_events(None, None)
     times = pairs.times_ms(steps)
     return (t1 - t0) * 1e3 / steps, sum(times) / len(times), times
@@ -424,6 +432,7 @@ def kv_transfer(torch, pa, workloads, steps, warmup, flush=None):
     trajectories between decode workers), and one turn's new tokens of the 16-sequence
     prefill-append batch (the per-turn hand-off from prefill to decode pool, Eq. 3)."""
     import numpy as np
+    from paper_2609_35158_amd import binding as bd
     out = []
     for name, gen, whole in (("kv-transfer-full-context", lambda: workloads.qwen3_8b_decode("cuda"), True),
                              ("kv-transfer-turn", lambda: workloads.qwen3_8b_prefill_append("cuda"), False)):
@@ -450,13 +459,30 @@ def kv_transfer(torch, pa, workloads, steps, warmup, flush=None):
         unpack = lambda hook: (hook(), pa.kv_unpack(buf, kp_b, vp_b, bt_b, st_d, cu_d, max_q, max_kv))
         _, ms_pack, _ = run_timed(torch, pa, pack, steps, warmup, flush)
         _, ms_unpack, _ = run_timed(torch, pa, unpack, steps, warmup, flush)
+        # the same bytes as one contiguous buffer copy (pearl_hbm_copy), equally cold: what a
+        # transfer of this size can reach when nothing is paged
+        dst = torch.empty_like(buf)
+        ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+        for i in range(warmup + steps):
+            if flush:
+                flush()
+            if i >= warmup:
+                ev[i - warmup][0].record()
+            bd.hbm_copy(buf, dst)
+            if i >= warmup:
+                ev[i - warmup][1].record()
+        torch.cuda.synchronize()
+        ms_plain = sum(a.elapsed_time(b) for a, b in ev) / steps
+        del dst
         moved = 2 * buf.numel() * 2            # read + write, bytes
         e = {"workload": name, "mode": "kv-transfer", "tokens": total, "buffer_bytes": buf.numel() * 2,
              "pack_ms": round(ms_pack, 5), "unpack_ms": round(ms_unpack, 5),
              "pack_GBps": round(moved / (ms_pack * 1e-3) / 1e9, 1),
-             "unpack_GBps": round(moved / (ms_unpack * 1e-3) / 1e9, 1)}
+             "unpack_GBps": round(moved / (ms_unpack * 1e-3) / 1e9, 1),
+             "plain_copy_GBps": round(moved / (ms_plain * 1e-3) / 1e9, 1)}
         e["frac_hbm_pack"] = round(e["pack_GBps"] / HBM_PEAK_GBPS, 4)
         e["frac_hbm_unpack"] = round(e["unpack_GBps"] / HBM_PEAK_GBPS, 4)
+        e["frac_hbm_plain_copy"] = round(e["plain_copy_GBps"] / HBM_PEAK_GBPS, 4)
         log("bench:   %s" % json.dumps(e))
         out.append(e)
         del case, kp_b, vp_b, buf, bt_b, perm
