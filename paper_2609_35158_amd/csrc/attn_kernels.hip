@@ -936,13 +936,19 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
   // One instruction stream for every M phase (no joins of differently allocated copies): M(0)
   // adds P = 0 times a zero-filled V buffer 2, and M(n) computes an S that no V phase reads.
   // R = j % 3: K(j) sits in K buffer R and V(j - 1) in V buffer (R + 2) % 3.
-  auto phase_m = [&](auto r_c) {
+  // The first kLead operands (V^T reads) of an M phase are read at the end of the softmax phase
+  // before it, so that their latency passes while the wave waits at the barrier.
+  bf16x8 ring[kLead];
+  auto prefetch = [&](auto r_c) {
+    constexpr int R = decltype(r_c)::value;
+#pragma unroll
+    for (int d = 0; d < kLead; ++d) ring[d] = operand(d, kbuf(R), vbuf((R + 2) % 3));
+  };
+  auto phase_m = [&](auto r_c, bool prefetched) {
     constexpr int R = decltype(r_c)::value;
     const char* kb_ = kbuf(R);
     const char* vb_ = vbuf((R + 2) % 3);
-    bf16x8 ring[kLead];
-#pragma unroll
-    for (int d = 0; d < kLead; ++d) ring[d] = operand(d, kb_, vb_);
+    if (!prefetched) prefetch(r_c);
 #pragma unroll
     for (int i = 0; i < NM; ++i) {
       const bf16x8 op = ring[i % kLead];
@@ -1023,17 +1029,15 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     }
     l_run += psum;
   };
-  // end of phase t: wait for this wave's copies that phase t + 1 reads (before M(j) of group A,
-  // j = (t + 1) / 2: K(j) and V(j - 1), the pair j - 2; those of the pair j - 1 stay in flight),
-  // drain the LDS reads, and pass the barrier without the release fence of __syncthreads (which
-  // would drain every copy)
+  // end of phase t: at t = 2i, wait for this wave's copies of V(i) and everything before it (K(i + 1)
+  // among them), which M(i + 1) reads from phase 2i + 2 on and the softmax phase before it reads
+  // ahead (the copy of K(i + 2), issued since, stays in flight); then drain the LDS reads and pass
+  // the barrier without the release fence of __syncthreads (which would drain every copy)
   constexpr int P = DT::NDMA;                       // DMA instructions per tensor and stage
   auto end_phase = [&](int t) {
-    if ((t & 1) != 0) {
-      const int j = (t + 1) >> 1;
-      const int later = (j + 1 < n) + (j < n);      // the pair j - 1: K(j + 1), V(j)
-      if (later == 2) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(2 * P));
-      else if (later == 1) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(P));
+    if ((t & 1) == 0) {
+      const int i = t >> 1;
+      if (i + 2 < n) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(P));   // K(i + 2) stays in flight
       else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
     }
     __builtin_amdgcn_s_waitcnt(PEARL_LGKMCNT0);
@@ -1067,26 +1071,30 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     // phases 2j, 2j + 1 for j < n: M(j), V(j); then M(n) and an empty phase.  The K rows of the
     // pair follow the MFMAs of M(j), the V rows open V(j), and the block-table entry of the next K
     // rows is read during V(j).
-    auto step = [&](auto r_c, int j) {
-      phase_m(r_c);
+    auto step = [&](auto r_c, int j, auto first_c) {
+      constexpr int R = decltype(r_c)::value;
+      phase_m(r_c, !decltype(first_c)::value);
       copy_k(r_c, j);
       end_phase(2 * j);
       copy_v(r_c, j);
       pid_v = pid_k;
       if (j + 3 < n) pid_k = page_of(j + 3);
       phase_v(j);
+      prefetch(std::integral_constant<int, (R + 1) % 3>{});
       end_phase(2 * j + 1);
     };
-    int j = 0;
+    using F = std::false_type;
+    step(I0{}, 0, std::true_type{});                // n >= 1
+    int j = 1;
     for (; j + 3 <= n; j += 3) {
-      step(I0{}, j);
-      step(I1{}, j + 1);
-      step(I2{}, j + 2);
+      step(I1{}, j, F{});
+      step(I2{}, j + 1, F{});
+      step(I0{}, j + 2, F{});
     }
-    if (j < n) { step(I0{}, j); ++j; }
-    if (j < n) { step(I1{}, j); ++j; }
+    if (j < n) { step(I1{}, j, F{}); ++j; }
+    if (j < n) { step(I2{}, j, F{}); ++j; }
     const int r = n % 3;                            // j == n
-    if (r == 0) phase_m(I0{}); else if (r == 1) phase_m(I1{}); else phase_m(I2{});
+    if (r == 0) phase_m(I0{}, true); else if (r == 1) phase_m(I1{}, true); else phase_m(I2{}, true);
     end_phase(2 * n);
     end_phase(2 * n + 1);
   } else {
@@ -1101,8 +1109,9 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
       copy_k(r_c, j);
       if (j + 3 < n) pid_n = page_of(j + 3);
       phase_v(j - 1);
+      prefetch(r_c);
       end_phase(2 * j);
-      phase_m(r_c);
+      phase_m(r_c, true);
       copy_v(r_c, j);
       pair_done();
       end_phase(2 * j + 1);
@@ -1110,7 +1119,7 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     copy_k(I0{}, 0);
     if (3 < n) pid_n = page_of(3);
     end_phase(0);
-    phase_m(I0{});
+    phase_m(I0{}, false);
     copy_v(I0{}, 0);
     pair_done();
     end_phase(1);
