@@ -801,6 +801,11 @@ def _record_current(e):
     return bool(e.get("sources")) and h.hexdigest() == e.get("sources_sha256")
 
 
+# the timed (dominant) kernel of each kind of step; decode batches of the benchmark are planned
+# inside the decode kernel
+KERNEL_OF = {"decode": "decode_kernel<128>", "prefill": "attn_kernel<128, 1>", "mixed": "attn_kernel<128, 3>"}
+
+
 def measured_traffic(kernel, workload):
     """HBM bytes per launch recorded from the rocprofv3 counter passes, or None when no record
     exists or the kernel source changed since the counters were taken."""
@@ -922,14 +927,14 @@ def main():
         },
         "hbm_tbps_step": round(nbytes / (ms_step * 1e-3) / 1e12, 4),
         "roofline": dict({
-            "kernel": "attn_kernel<128, decode> (decode split items)",
+            "kernel": "decode_kernel<128> (decode planned, split, merged and appended in one kernel)",
             "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBPS, 4),
-            "traffic": measured_traffic("attn_kernel<128>", "qwen3-8b-decode-b64"),
+            "traffic": measured_traffic(KERNEL_OF["decode"], "qwen3-8b-decode-b64"),
             "algorithmic_bytes": nbytes, "kernel_ms": round(ms_kernel, 5),
             "frac_of_measured": vs_measured(achieved),
             "tflops": round(flops / (ms_kernel * 1e-3) / 1e12, 2),
-            "counters": kernel_counters("attn_kernel<128>", "qwen3-8b-decode-b64"),
+            "counters": kernel_counters(KERNEL_OF["decode"], "qwen3-8b-decode-b64"),
         }, **launch_stats(launches)),
         "timing": {"input_replicas": len(reps),
                    "what": "consecutive steps use different copies of the inputs (others >= 1 GiB between two "
@@ -997,14 +1002,16 @@ def main():
                           "kv_append_ms": round(ms_a, 5),
                           "kv_append_GBps": round(append_bytes(c) / (ms_a * 1e-3) / 1e9, 1),
                           "input_replicas": len(reps)})
+            entry["kernel"] = KERNEL_OF[mode]
+            entry["traffic"] = measured_traffic(KERNEL_OF[mode], name)
+            cnt = kernel_counters(KERNEL_OF[mode], name)
+            entry["counters"] = cnt
             if mode == "decode":
                 entry["tok_s"] = round(c.batch / (ms_s * 1e-3), 1)
                 entry["frac_hbm"] = round(entry["GBps"] / HBM_PEAK_GBPS, 4)
                 entry["frac_of_measured"] = vs_measured(entry["GBps"])
             elif mode == "prefill":
                 entry["frac_mfma"] = round(entry["TFLOPs"] / BF16_PEAK_TFLOPS, 4)
-                cnt = kernel_counters("attn_kernel<128>", name)
-                entry["counters"] = cnt
                 if cnt:
                     # the published peak is quoted at 2400 MHz; the same MFMA units at the clock the
                     # counters measured over this kernel
