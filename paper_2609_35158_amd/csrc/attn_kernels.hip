@@ -243,14 +243,15 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
     s_split_keys = (int)S;
     // Mixed launches: how many workgroups take prefill items first (the others take decode items
-    // first).  Decode stays bound by HBM on fewer compute units, so prefill gets somewhat more
-    // than its share of the estimated work: 1.4 x share, in prefill and decode key-units weighted
-    // 3 : 2 as above.
+    // first): 1.1 x prefill's share of the estimated work, in prefill and decode key-units
+    // weighted 3 : 2 as above.  Decode on fewer compute units draws less bandwidth per unit than
+    // the whole chip does, and a prefill tile left for the end of a launch holds one workgroup
+    // far longer than a decode split, so prefill gets a little more than its share.
     int pre_first = 0;
     if (p.mixed_grid > 0) {
       const long long pu = 3LL * (long long)s_pre_keys * H;
       const long long du = 2LL * (long long)s_dec_keys * H;
-      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (14LL * p.mixed_grid * pu) / (10 * (pu + du)))
+      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (11LL * p.mixed_grid * pu) / (10 * (pu + du)))
                               : p.mixed_grid;
     }
     s_pre_first = pre_first;
@@ -492,300 +493,19 @@ template <int D, int KEYS = kKeysPerStage> struct DmaTile {
 // lane-local apart from one exchange with lane l^32, which holds the row's other keys.
 // A split item (entry e, code = tile | split << 16) covers only its key range and writes the
 // unnormalised (o~, m, l) of its rows to partial slot e * H_kv + g for the prefill merge.
-// ------------------------------------------------------------------------------------------------
-// kHoistV (prefill-only kernels, which have registers and instruction cache to spare): read the
-// first dim block's V^T operands before the softmax (16 more VGPRs) and unroll the stage loop over
-// the three buffers.  The mixed kernel, short of both, selects the buffers at run time instead,
-// which keeps its code small (measured faster there; the unrolled form is faster alone).
-// Stages travel by LDS-DMA into three DmaTile buffers per tensor (kb*, vb*), two stages ahead.
-template <int D, bool kHoistV>
-__device__ __forceinline__ void prefill_tile(const AttnArgs& a, int e, int b, int code, int g, int split_keys,
-                                             char* kb0, char* kb1, char* kb2, char* vb0, char* vb1, char* vb2) {
-  constexpr int KB = D / 16;                        // 16-wide k blocks of the QK product
-  constexpr int MB = D / 32;                        // 32-wide dim blocks of the PV product
-  using DT = DmaTile<D>;
-  constexpr int RB = DT::RB;
-  // the unrolled loop names each buffer by a constant; the run-time loop needs contiguous
-  // buffers (k/vb1 = k/vb0 + BYTES, k/vb2 = k/vb0 + 2 * BYTES), which its caller provides
-  auto kbuf = [&](int buf) { return kHoistV ? (buf == 0 ? kb0 : (buf == 1 ? kb1 : kb2)) : kb0 + buf * DT::BYTES; };
-  auto vbuf = [&](int buf) { return kHoistV ? (buf == 0 ? vb0 : (buf == 1 ? vb1 : vb2)) : vb0 + buf * DT::BYTES; };
-
-  // the thread index passes through an empty asm, so the per-lane offsets derived from it are
-  // computed per item: hoisted out of the mixed kernel's item loop, they stayed live across the
-  // decode items too and pushed that kernel past its registers
-  int tid = threadIdx.x;
-  __asm__ volatile("" : "+v"(tid));
-  const int lane = tid & 63, half = lane >> 5;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index (uniform)
-  const SeqInfo si = a.seqinfo[b];
-  const int G = a.group;
-  const int tile = code & 0xffff, split = code >> 16;
-  const int t0 = tile * a.tokens_per_tile;
-  const int t_end = min(t0 + a.tokens_per_tile, si.q_len);
-  const int ctx = si.ctx_len;
-  const int kv_needed = ctx + t_end;
-  const int rho = 32 * w + (lane & 31);
-  const int tok = t0 + rho / G;
-  const int hh = rho - (rho / G) * G;
-  const int h = g * G + hh;
-  const bool row_ok = tok < t_end;
-  const int row_limit = ctx + tok;                  // last visible key of this row
-  const int wave_min_limit = ctx + t0 + (32 * w) / G;
-  const int H_q = a.num_q_heads, H_kv = a.num_kv_heads;
-  const size_t head_stride = (size_t)kPage * D;     // elements per (page, kv-head) block
-  const float c = a.scale_log2;
-
-  bf16x8 qop[KB];
-  {
-    const uint16_t* qrow = a.q + ((size_t)(si.q_start + (row_ok ? tok : t0)) * H_q + h) * D + 8 * half;
-#pragma unroll
-    for (int kb = 0; kb < KB; ++kb) qop[kb] = row_ok ? as_bf16x8(ld16(qrow + 16 * kb)) : zero_bf16x8();
-  }
-
-  f32x16 oacc[MB];
-#pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) oacc[mb][r] = 0.f;
-  float m_run = -INFINITY, l_run = 0.f;
-
-  const int n_steps = (kv_needed + kKeysPerStage - 1) / kKeysPerStage;
-  const int n_split = tile_splits(ctx, t0, split_keys);
-  const int step_begin = split * (split_keys / kKeysPerStage);
-  const int step_end = split + 1 < n_split ? step_begin + split_keys / kKeysPerStage : n_steps;
-
-  const ConstI32Ptr bt_c = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
-  const int last_pidx = (kv_needed - 1) / kPage;
-  // per-lane byte offsets of the K operand rows (Q.K), of the V^T transposing reads (P.V; rows
-  // krow and krow + 8 of each 16-key half) and of the slots this lane fills by DMA
-  const int gi = lane >> 4, jl = lane & 15;
-  const int krow = 4 * (gi >> 1) + (jl >> 2);
-  const int dcol = 16 * (gi & 1) + 4 * (jl & 3);
-  int koff[KB], voff[2][MB], goff[DT::NDMA];
-#pragma unroll
-  for (int kb = 0; kb < KB; ++kb) koff[kb] = (lane & 31) * RB + (((2 * kb + half) ^ DT::swz(lane & 15)) << 4);
-#pragma unroll
-  for (int sec = 0; sec < 2; ++sec)
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int r = krow + 8 * sec;
-      voff[sec][mb] = r * RB + ((((32 * mb + dcol) >> 3) ^ DT::swz(r)) << 4) + (jl & 1) * 8;
-    }
-#pragma unroll
-  for (int i = 0; i < DT::NDMA; ++i) {
-    const int r = DT::RPW * w + DT::RPI * i + lane / DT::CPR;   // stage row of this lane's slot
-    goff[i] = (r % kPage) * RB + (((lane % DT::CPR) ^ DT::swz(r)) << 4);
-  }
-  // This wave's rows of stage `step` (one page) by LDS-DMA.  Stages past the last needed key
-  // re-read a valid page; V rows past it come from the workspace's zero block (K rows there are
-  // always masked).
-  const char* zero_src = reinterpret_cast<const char*>(a.ws_hdr + kHdrZero);
-  auto dma_stage = [&](int step, int buf) {
-    const int pidx = min((step * kKeysPerStage + DT::RPW * w) / kPage, last_pidx);
-    const int page = clamp_page(bt_c[pidx], a.num_pages);
-    const size_t base = (((size_t)page * H_kv + g) * head_stride) * 2;
-    const char* ksrc = reinterpret_cast<const char*>(a.k_pool) + base;
-    const char* vsrc = reinterpret_cast<const char*>(a.v_pool) + base;
-#pragma unroll
-    for (int i = 0; i < DT::NDMA; ++i) {
-      const int key = step * kKeysPerStage + DT::RPW * w + DT::RPI * i + lane / DT::CPR;
-      const int row0 = DT::RPW * w + DT::RPI * i;
-      lds_dma16_untracked(ksrc + goff[i], kbuf(buf) + row0 * RB);
-      lds_dma16_untracked(key < kv_needed ? vsrc + goff[i] : zero_src, vbuf(buf) + row0 * RB);
-    }
-  };
-  auto compute = [&](int step, int buf) {
-      const char* kb_ = kbuf(buf);
-      const char* vb_ = vbuf(buf);
-      // byte offsets of a K operand row (sub-tile st, k block kb) and of a V^T transposing read
-      // (sub-tile st, 16-key half kk, dim block mb, row half sec)
-      auto koffset = [&](int st, int kb) { return 32 * st * RB + koff[kb]; };
-      auto voffset = [&](int st, int kk, int mb, int sec) { return (32 * st + 16 * kk) * RB + voff[sec][mb]; };
-      const int k0 = step * kKeysPerStage;
-
-      // S^T = K Q^T for two 32-key sub-tiles
-      f32x16 s[2];
-      const f32x16 zero16 = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int st = 0; st < 2; ++st) {
-#pragma unroll
-        for (int kb = 0; kb < KB; ++kb) {
-          const bf16x8 kop = *reinterpret_cast<const bf16x8*>(kb_ + koffset(st, kb));
-          s[st] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kop, qop[kb], kb == 0 ? zero16 : s[st], 0, 0, 0);
-        }
-      }
-      // with kHoistV the V^T operands of the first 32-dim block are read now, so their LDS
-      // latency hides behind the softmax instead of stalling the first P.V products
-      bf16x8 vfirst[2][2];
-      if constexpr (kHoistV) {
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            vfirst[st][kk] = concat_tr(lds_read_tr(vb_, voffset(st, kk, 0, 0)), lds_read_tr(vb_, voffset(st, kk, 0, 1)));
-          }
-      }
-      // causal mask (only on steps that reach past some row's last visible key); the empty asm
-      // keeps this a real branch: the compiler would otherwise evaluate the mask on every step
-      if (k0 + kKeysPerStage - 1 > wave_min_limit) {
-        __asm__ volatile("" ::);
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const int key = k0 + 32 * st + (r & 3) + 8 * (r >> 2) + 4 * half;
-            if (key > row_limit) s[st][r] = -INFINITY;
-          }
-      }
-      // online softmax (base 2).  The weights are first taken against the running maximum m
-      // without looking for this stage's maximum; that is exact (any m gives the same softmax)
-      // as long as no weight exceeds 2^kMaxLag, which the lane's sum of its 32 weights bounds.
-      // Otherwise (the first stage of an item, where m is still -inf, or scores jumping more than
-      // kMaxLag above m) the stage is redone with the row maximum, and m moves to it only when it
-      // exceeds m by more than kMaxLag, so the O rescale is rare too.  A NaN sum (a masked key
-      // against m = -inf) also takes the redo.
-      float ps0 = 0.f, ps1 = 0.f;
-      bf16x8 pop[2][2];
-#pragma unroll
-      for (int st = 0; st < 2; ++st)
-#pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_run));
-          if (r & 1) ps1 += pv; else ps0 += pv;
-          pop[st][r >> 3][r & 7] = (__bf16)pv;
-        }
-      float psum = ps0 + ps1;
-      if (__ballot(!(psum <= kMaxWeightSum))) {
-        __asm__ volatile("" ::);                   // a real branch
-        float mx = s[0][0];
-#pragma unroll
-        for (int r = 1; r < 16; ++r) mx = fmaxf(mx, s[0][r]);
-#pragma unroll
-        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, s[1][r]);
-        mx = xor32_max(mx);
-        const bool grow = mx * c > m_run + kMaxLag;
-        const float m_new = grow ? mx * c : m_run;
-        const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
-        ps0 = ps1 = 0.f;
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int r = 0; r < 16; ++r) {
-            const float pv = fexp2(__builtin_fmaf(s[st][r], c, -m_new));
-            if (r & 1) ps1 += pv; else ps0 += pv;
-            pop[st][r >> 3][r & 7] = (__bf16)pv;
-          }
-        psum = ps0 + ps1;
-        l_run *= alpha;
-        if (__ballot(grow)) {
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-            for (int r = 0; r < 16; ++r) oacc[mb][r] *= alpha;
-        }
-        m_run = m_new;
-      }
-      l_run += psum;
-      // O^T += V^T P^T
-#pragma unroll
-      for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-        for (int st = 0; st < 2; ++st)
-#pragma unroll
-          for (int kk = 0; kk < 2; ++kk) {
-            bf16x8 vop;
-            if (kHoistV && mb == 0) {
-              vop = vfirst[st][kk];
-            } else {
-              vop = concat_tr(lds_read_tr(vb_, voffset(st, kk, mb, 0)), lds_read_tr(vb_, voffset(st, kk, mb, 1)));
-            }
-            oacc[mb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vop, pop[st][kk], oacc[mb], 0, 0, 0);
-          }
-  };
-
-  // stage s sits in buffer (s - step_begin) % 3; its copy is issued two stages ahead, and the
-  // barrier closing stage s waits for the copy of stage s+1 only (the one of stage s+2 stays
-  // in flight).  The barrier is issued without the release fence of __syncthreads, which would
-  // drain every copy; all LDS reads of the stage have been consumed by then.
-  constexpr int kCopies = 2 * DT::NDMA;           // DMA instructions per stage and wave
-  auto close_stage = [&](bool copy_in_flight) {
-    if (copy_in_flight) __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(kCopies));
-    else __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));
-    __asm__ volatile("s_barrier" ::: "memory");
-  };
-  // the prologue waits for everything (both first copies and this item's Q loads), so the
-  // compiler knows no load of its own is outstanding inside the loop
-  dma_stage(step_begin, 0);
-  if (step_begin + 1 < step_end) dma_stage(step_begin + 1, 1);
-  close_stage(false);
-  if constexpr (kHoistV) {
-    for (int step = step_begin; step < step_end; step += 3) {
-      if (step + 2 < step_end) dma_stage(step + 2, 2);
-      compute(step, 0);
-      close_stage(step + 2 < step_end);
-      if (step + 1 >= step_end) break;
-      if (step + 3 < step_end) dma_stage(step + 3, 0);
-      compute(step + 1, 1);
-      close_stage(step + 3 < step_end);
-      if (step + 2 >= step_end) break;
-      if (step + 4 < step_end) dma_stage(step + 4, 1);
-      compute(step + 2, 2);
-      close_stage(step + 4 < step_end);
-    }
-  } else {
-    for (int step = step_begin, buf = 0; step < step_end; ++step, buf = buf == 2 ? 0 : buf + 1) {
-      if (step + 2 < step_end) dma_stage(step + 2, buf == 0 ? 2 : buf - 1);
-      compute(step, buf);
-      close_stage(step + 2 < step_end);
-    }
-  }
-
-  // epilogue: combine the two half-row sums; a split item stores its fp32 partial state
-  const float l_tot = xor32_add(l_run);
-  if (row_ok && n_split > 1) {
-    const size_t prow = (size_t)(e * H_kv + g) * kRowsPerTile + rho;
-    float* po = a.part_pre_o + prow * D;
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq)
-        *reinterpret_cast<f32x4*>(po + 32 * mb + 8 * rq + 4 * half) =
-            f32x4{oacc[mb][4 * rq + 0], oacc[mb][4 * rq + 1], oacc[mb][4 * rq + 2], oacc[mb][4 * rq + 3]};
-    if (half == 0) {
-      a.part_pre_ml[2 * prow] = m_run;
-      a.part_pre_ml[2 * prow + 1] = l_tot;
-    }
-  } else if (row_ok) {
-    // normalise, store bf16 O and fp32 LSE
-    const float inv = 1.0f / l_tot;
-    uint16_t* orow = a.out + ((size_t)(si.q_start + tok) * H_q + h) * D;
-#pragma unroll
-    for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-      for (int rq = 0; rq < 4; ++rq) {
-        const int dim = 32 * mb + 8 * rq + 4 * half;
-        u32x2 pk;
-        pk[0] = (uint32_t)bf16_bits(oacc[mb][4 * rq + 0] * inv) | ((uint32_t)bf16_bits(oacc[mb][4 * rq + 1] * inv) << 16);
-        pk[1] = (uint32_t)bf16_bits(oacc[mb][4 * rq + 2] * inv) | ((uint32_t)bf16_bits(oacc[mb][4 * rq + 3] * inv) << 16);
-        *reinterpret_cast<u32x2*>(orow + dim) = pk;
-      }
-    if (half == 0 && a.lse) a.lse[(size_t)(si.q_start + tok) * H_q + h] = (m_run + flog2(l_tot)) * kLn2;
-  }
-}
-
-// ------------------------------------------------------------------------------------------------
-// Prefill-append work item for the prefill-only kernel, with the matrix and vector work of the two
-// waves on each SIMD overlapped.  Same item, tile, operand layouts and softmax as prefill_tile; the
-// difference is the schedule.  The 8 waves form two groups, waves 0-3 and waves 4-7 (the waves
-// w and w + 4 share a SIMD), and the item runs in phases separated by workgroup barriers.  In each
-// of its phases a wave does either
+//
+// Schedule (prefill-only and mixed kernels): the matrix and vector work of the two waves on each
+// SIMD overlap.  The 8 waves form two groups, waves 0-3 and waves 4-7 (the waves w and w + 4 share
+// a SIMD), and the item runs in phases separated by workgroup barriers.  In each of its phases a
+// wave does either
 //   M(j): S(j) = K(j) Q^T and O += V(j-1)^T P(j-1)   (32 MFMAs at d = 128, no dependence between
 //         the two products), or
 //   V(j): the online softmax of S(j), giving P(j)    (exp, scale and sums on the vector ALU),
 // alternating M(0) V(0) M(1) V(1) ... M(n); group B runs one phase behind group A.  In every phase
 // one wave of each SIMD therefore issues MFMAs while the other runs its softmax, so the matrix core
 // works through the vector phase of the other wave instead of waiting for it.
-// Stages travel by LDS-DMA as before: K(j) into K buffer j % 3, V(j) into V buffer j % 3.  K(j) is
+// Stages travel by LDS-DMA into three DmaTile buffers per tensor: K(j) into K buffer j % 3, V(j)
+// into V buffer j % 3.  K(j) is
 // read in phases 2j and 2j+1, V(j) in phases 2j+2 and 2j+3.  Each wave copies its rows of K(j+2)
 // and V(j+1) (the pair j) in phases 2j and 2j+1, into buffers last read in phase 2j-1: half of the
 // DMA instructions right after its MFMAs of M(j), the other half at the start of its adjacent
@@ -971,8 +691,14 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     for (int i = 0; i < DT::NDMA; ++i)
       if (j + 1 < n) dma_one(j + 1, true, pid_v, vbuf((R + 1) % 3), i);
   };
-  // V(j), 0 <= j < n: causal mask (stages reaching past some row's last key), then the online
-  // softmax with a lagging maximum, exactly as in prefill_tile
+  // V(j), 0 <= j < n: causal mask (only on stages that reach past some row's last visible key; the
+  // empty asm keeps that a real branch), then the online softmax (base 2).  The weights are first
+  // taken against the running maximum m without looking for this stage's maximum; that is exact
+  // (any m gives the same softmax) as long as no weight exceeds 2^kMaxLag, which the lane's sum of
+  // its 32 weights bounds.  Otherwise (the first stage of an item, where m is still -inf, or
+  // scores jumping more than kMaxLag above m) the stage is redone with the row maximum, and m
+  // moves to it only when it exceeds m by more than kMaxLag, so the O rescale is rare too.  A NaN
+  // sum (a masked key against m = -inf) also takes the redo.
   auto phase_v = [&](int j) {
     const int k0 = (step_begin + j) * SK;
     if (k0 + SK - 1 > wave_min_limit) {
@@ -1133,7 +859,8 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
     if (j <= n) { step(I2{}, j); ++j; }
   }
 
-  // epilogue (as in prefill_tile): combine the half-row sums; a split item stores its partial state
+  // epilogue: combine the two half-row sums; a split item stores its fp32 partial state, a whole
+  // item normalises and stores bf16 O and the fp32 LSE
   const float l_tot = xor32_add(l_run);
   if (row_ok && n_split > 1) {
     const size_t prow = (size_t)(e * H_kv + g) * kRowsPerTile + rho;
@@ -1690,8 +1417,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
           // workgroup runs one item at a time, and items are separated by a drained barrier)
           constexpr int B = DmaTile<D>::BYTES;
           static_assert(6 * B <= Lds<D, NW, kKinds>::bytes, "stage buffers fit the shared region");
-          prefill_tile<D, false>(a, e, en.x, en.y, g, split_keys, smem, smem + B, smem + 2 * B,
-                                       smem + 3 * B, smem + 4 * B, smem + 5 * B);
+          prefill_tile_pp<D>(a, e, en.x, en.y, g, split_keys, smem, smem + 3 * B);
         }
       }
     } else {
