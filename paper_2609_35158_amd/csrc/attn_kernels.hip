@@ -105,12 +105,12 @@ constexpr float kMaxWeightSum = 256.0f;             // 2^kMaxLag
 // in attn_kernel.
 template <int D, int NW, int kKinds> struct Lds {
   // prefill stages travel by LDS-DMA into six stage buffers (three K, three V): separate arrays
-  // in prefill-only kernels, carved from the region of the decode V buffers in the mixed kernel
+  // in prefill-only kernels, carved from the region of the decode stages in the mixed kernel
   static constexpr int prefill_bytes = (kKinds == 3) ? 6 * kKeysPerStage * D * 2 : 0;
-  static constexpr int decode_v_bytes = NW * 2 * (2 * kPage * D * 2);   // per-wave double buffer
+  static constexpr int decode_stage_bytes = NW * 2 * (2 * kPage * D * 2);   // per-wave K+V double buffer
   static constexpr int merge_bytes = NW * 8 * D * 4 + 2 * NW * 8 * 4;
-  // decode-only kernels keep their V buffers in separate arrays; the mixed kernel carves them here
-  static constexpr int decode_bytes = (kKinds == 3) ? decode_v_bytes : 0;
+  // decode-only kernels keep their stages in separate arrays; the mixed kernel carves them here
+  static constexpr int decode_bytes = (kKinds == 3) ? decode_stage_bytes : 0;
   static constexpr int bytes0 = prefill_bytes > decode_bytes ? prefill_bytes : decode_bytes;
   static constexpr int bytes = bytes0 > 16 ? bytes0 : 16;
 };
@@ -243,22 +243,21 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
     s_split_keys = (int)S;
     // Mixed launches: how many workgroups take prefill items first (the others take decode items
-    // first): 1.1 x prefill's share of the estimated work, in prefill and decode key-units
-    // weighted 3 : 2 as above.  Decode on fewer compute units draws less bandwidth per unit than
-    // the whole chip does, and a prefill tile left for the end of a launch holds one workgroup
-    // far longer than a decode split, so prefill gets a little more than its share.
+    // first): 1.35 x prefill's share of the estimated work, in prefill and decode key-units
+    // weighted 3 : 2 as above.  A prefill tile left for the end of a launch holds one workgroup
+    // far longer than a decode split, so prefill gets more than its share.
     int pre_first = 0;
     if (p.mixed_grid > 0) {
       const long long pu = 3LL * (long long)s_pre_keys * H;
       const long long du = 2LL * (long long)s_dec_keys * H;
-      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (11LL * p.mixed_grid * pu) / (10 * (pu + du)))
+      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (27LL * p.mixed_grid * pu) / (20 * (pu + du)))
                               : p.mixed_grid;
     }
     s_pre_first = pre_first;
     // Decode split size: about kDecItemsPerCU items per compute unit over the launch's actual
     // pages, a multiple of 16 pages, at least the host's bound and at most kMaxPagesPerSplit.
-    // Splits of at least kDecLongSplitPages pages (8 page pairs per wave) while that still leaves
-    // 2 items per compute unit: a wave's first pair of an item waits unhidden, so short splits
+    // Splits of at least kDecLongSplitPages pages (16 pages per wave) while that still leaves
+    // 2 items per compute unit: a wave's first page of an item waits unhidden, so short splits
     // pay it often.
     long long pps = p.pages_per_split;
     if (s_dec_pages > 0) {
@@ -429,29 +428,39 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   }
 }
 
-// 16 bytes per lane from global memory straight into LDS: lane l writes lds_base + 16 l.
-__device__ __forceinline__ void lds_dma16(const void* g, char* lds_base) {
-  __builtin_amdgcn_global_load_lds(g, (LDS_AS void*)((LDS_AS char*)(lds_base)), 16, 0, 0);
-}
-
-// The same copy issued as inline assembly, which the compiler does not track: it then inserts
-// no waits of its own for it (it would wait for every copy in flight before any LDS read), and
-// the caller waits with explicit vmcnt counts.  The compiler's own vmcnt waits stay correct,
-// because copies it does not know about can only make them wait longer.  The LDS base goes
-// through M0, which the sequence saves and restores (the copy reads it at issue, one wait state
-// after it is written).  lds_base must be uniform across the wave.
+// 16 bytes per lane from global memory straight into LDS (lane l writes lds_base + 16 l), issued
+// as inline assembly, which the compiler does not track: it then inserts no waits of its own for
+// it (it would wait for every copy in flight before any LDS read), and the caller waits with
+// explicit vmcnt counts.  The compiler's own vmcnt waits stay correct, because copies it does
+// not know about can only make them wait longer.  The LDS base goes through M0, which the
+// sequence saves and restores (the copy reads it at issue, one wait state after it is written).
+// lds_base must be uniform across the wave.  kOnce: the load is marked non-temporal (nt), for
+// bytes read once per launch.
+template <bool kOnce = false>
 __device__ __forceinline__ void lds_dma16_untracked(const void* g, const char* lds_base) {
   const unsigned lds = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)((LDS_AS const char*)lds_base));
   unsigned saved;
-  __asm__ volatile(
-      "s_mov_b32 %0, m0\n\t"
-      "s_mov_b32 m0, %2\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off\n\t"
-      "s_mov_b32 m0, %0"
-      : "=&s"(saved)
-      : "v"(g), "s"(lds)
-      : "memory");
+  if constexpr (kOnce) {
+    __asm__ volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off nt\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(g), "s"(lds)
+        : "memory");
+  } else {
+    __asm__ volatile(
+        "s_mov_b32 %0, m0\n\t"
+        "s_mov_b32 m0, %2\n\t"
+        "s_nop 0\n\t"
+        "global_load_lds_dwordx4 %1, off\n\t"
+        "s_mov_b32 m0, %0"
+        : "=&s"(saved)
+        : "v"(g), "s"(lds)
+        : "memory");
+  }
 }
 
 // vmcnt(n) with the other counters left alone (gfx9 encoding: vmcnt in bits 3:0 and 15:14)
@@ -894,38 +903,50 @@ __device__ __forceinline__ void prefill_tile_pp(const AttnArgs& a, int e, int b,
 
 // ------------------------------------------------------------------------------------------------
 // Decode work item: one (sequence, kv-head g, split of pps pages; the planner chooses pps).  The
-// G q-heads of the group are the 16 columns of 16x16x32 MFMAs (columns >= G are zero), so each
-// K/V byte is loaded once for the whole group.  Wave w takes page pairs w, w+8, ... of the split:
-//   S^T (16 keys x heads) = K_page . Q^T          (A = K straight from HBM into registers)
-//   O^T (dims x heads)   += V^T . P^T over 32 keys (A = V^T read transposed from LDS)
-// V travels HBM -> LDS with 16-byte LDS-DMA loads (no VGPRs, no LDS store instructions) into a
-// per-wave double buffer; K is double-buffered in registers, so the next pair's loads are in
-// flight while the current pair is consumed.  Every load is unconditional: addresses stay inside
-// the split's own pages, and V rows of keys past the sequence end are fetched from a zeroed block
-// of the workspace so they add nothing to P.V (their scores are masked to -inf).  The 8 waves'
-// partial softmax states are merged through LDS; a sequence with one split writes its output
-// directly, otherwise the (o~, m, l) partial goes to the workspace.
+// G q-heads of the group are the 16 columns of the MFMA products (columns >= G are zero), so each
+// K/V byte is loaded once for the whole group.  Wave w takes pages w, w+8, ... of the split:
+//   S^T (16 keys x heads) = K_page . Q^T           (16x16x32 MFMA: A = K rows read from LDS)
+//   O^T (dims x heads)   += V^T . P^T over 16 keys (16x16x16 MFMA: A = V^T read transposed from LDS)
+// K and V travel HBM -> LDS by 16-byte LDS-DMA loads (no VGPRs, no LDS store instructions) into a
+// per-wave double buffer, so the next page's loads are in flight while the current page is
+// consumed.  Each DMA instruction moves whole key rows (1 KiB of consecutive bytes), marked
+// non-temporal: every K/V byte is read once per launch, and such full-line reads marked that way
+// reach a higher HBM rate than plain ones (K read straight into MFMA operand registers touched
+// half of each 128-byte line per instruction, which the non-temporal mark made slower).  Every
+// load is unconditional: addresses stay inside the split's own pages, and V rows of keys past the
+// sequence end are fetched from a zeroed block of the workspace so they add nothing to P.V
+// (their scores are masked to -inf).  The 8 waves' partial softmax states are merged through
+// LDS; a sequence with one split writes its output directly, otherwise the (o~, m, l) partial
+// goes to the workspace.
 //
-// V buffer layout: 32 rows (keys of the pair) x D/8 16-byte chunks, unpadded; chunk c of row r is
-// stored at chunk slot c ^ swz(r), which spreads the transpose reads over all LDS banks.
+// Stage layout (per wave): the page's K rows, then its V rows, kPage rows x D/8 16-byte chunks
+// each, unpadded.  Chunk c of K row r sits in slot c ^ kswz(r), so the 16 rows that one operand
+// read covers fall in 16 different 16-byte bank groups; chunk c of V row r sits in slot
+// c ^ vswz(r), which spreads the transposing reads over all LDS banks.
 // ------------------------------------------------------------------------------------------------
-template <int D> struct DecodeK {
-  static constexpr int KB = D / 32;                 // 32-wide k blocks of the QK product
-  u32x4 ka[KB], kb[KB];
-};
-
-template <int D> struct VTile {
+template <int D> struct PageTile {
   static constexpr int CPR = D / 8;                 // 16-byte chunks per key row
   static constexpr int ROWB = D * 2;                // bytes per key row
   static constexpr int RPI = 64 / CPR;              // rows written by one 64-lane DMA instruction
-  static constexpr int PAIR_BYTES = 2 * kPage * ROWB;
-  static constexpr int NDMA = 2 * kPage / RPI;      // DMA instructions per page pair
-  __device__ static __forceinline__ int swz(int r) {
+  static constexpr int TBYTES = kPage * ROWB;       // one tensor of one page
+  static constexpr int BYTES = 2 * TBYTES;          // K rows, then V rows
+  static constexpr int NDMA = kPage / RPI;          // DMA instructions per tensor and page
+  static constexpr int KB = D / 32;                 // 32-wide k blocks of the QK product
+  static constexpr int MB = D / 16;                 // 16-wide dim blocks of the PV product
+  __device__ static __forceinline__ int kswz(int r) {
+    // d = 128: 16 slots per row, one per row of the page; d = 64: 8 slots per row and rows 2i,
+    // 2i + 1 in opposite halves of the banks
+    if constexpr (D == 128) return r & 15;
+    else return (r >> 1) & 7;
+  }
+  __device__ static __forceinline__ int vswz(int r) {
     return (((r & 3) << 2) | (((r >> 2) & 1) << 1)) & (CPR - 1);
   }
-  // byte offset of (row r, 4-element group starting at dim d0) inside the buffer
-  __device__ static __forceinline__ int off(int r, int d0) {
-    return r * ROWB + (((d0 >> 3) ^ swz(r)) << 4) + ((d0 >> 2) & 1) * 8;
+  // byte offset of K row r, chunk c
+  __device__ static __forceinline__ int koff(int r, int c) { return r * ROWB + ((c ^ kswz(r)) << 4); }
+  // byte offset of (V row r, 4-element group starting at dim d0)
+  __device__ static __forceinline__ int voff(int r, int d0) {
+    return TBYTES + r * ROWB + (((d0 >> 3) ^ vswz(r)) << 4) + ((d0 >> 2) & 1) * 8;
   }
 };
 
@@ -938,111 +959,87 @@ struct NewRow {
   const uint16_t* v;
 };
 
+// Issues the copies of logical page p (physical page phys) of kv-head g into the stage at dst.
 // kNew: the item may hold the new row (decode_kernel); otherwise nr is ignored.
 template <int D, bool kNew>
-__device__ __forceinline__ void decode_issue(const AttnArgs& a, int phys_a, int phys_b, bool pb_ok, int pa,
-                                             int g, int kv, DecodeK<D>& K, char* vdst, const NewRow& nr) {
-  using VT = VTile<D>;
-  const int lane = threadIdx.x & 63, gi = lane >> 4, hh = lane & 15;
-  const size_t head_stride = (size_t)kPage * D;
-  const size_t ga = ((size_t)phys_a * a.num_kv_heads + g) * head_stride;
-  const size_t gb = ((size_t)phys_b * a.num_kv_heads + g) * head_stride;
-  const bool new_a = kNew && pa == nr.page && hh == nr.slot, new_b = kNew && pa + 1 == nr.page && hh == nr.slot;
-#pragma unroll
-  for (int kb = 0; kb < DecodeK<D>::KB; ++kb) {
-    const int off = hh * D + 32 * kb + 8 * gi;
-    K.ka[kb] = ld16(new_a ? nr.k + 32 * kb + 8 * gi : a.k_pool + ga + off);
-    K.kb[kb] = ld16(new_b ? nr.k + 32 * kb + 8 * gi : a.k_pool + gb + off);
-  }
+__device__ __forceinline__ void decode_issue(const AttnArgs& a, int phys, int p, int g, int kv, char* dst,
+                                             const NewRow& nr) {
+  using PT = PageTile<D>;
+  const int lane = threadIdx.x & 63;
+  const size_t blk = ((size_t)phys * a.num_kv_heads + g) * (size_t)(kPage * D);
   const uint16_t* zero = reinterpret_cast<const uint16_t*>(a.ws_hdr + kHdrZero);
+  const int slot = lane % PT::CPR;                  // chunk slot this lane fills
 #pragma unroll
-  for (int i = 0; i < VT::NDMA; ++i) {
-    const int r = i * VT::RPI + lane / VT::CPR;     // key row of the pair written by this lane
-    const int slot_c = lane % VT::CPR;              // chunk slot this lane fills
-    const int c = slot_c ^ VT::swz(r);              // global chunk stored there
-    const int pg = r >> 4, key = r & 15;            // pg is the same for every lane of a given i
-    const bool ok = (pg == 0 || pb_ok) && (pa + pg) * kPage + key < kv;
-    const bool is_new = kNew && pa + pg == nr.page && key == nr.slot;
-    const uint16_t* src = ok ? (is_new ? nr.v + c * 8 : a.v_pool + (pg ? gb : ga) + key * D + c * 8) : zero;
-    lds_dma16(src, vdst + i * 1024);
+  for (int i = 0; i < PT::NDMA; ++i) {
+    const int r = i * PT::RPI + lane / PT::CPR;     // key row of the page written by this lane
+    const bool is_new = kNew && p == nr.page && r == nr.slot;
+    const int ck = slot ^ PT::kswz(r);
+    lds_dma16_untracked<true>(is_new ? nr.k + ck * 8 : a.k_pool + blk + r * D + ck * 8, dst + i * 1024);
+  }
+#pragma unroll
+  for (int i = 0; i < PT::NDMA; ++i) {
+    const int r = i * PT::RPI + lane / PT::CPR;
+    const bool ok = p * kPage + r < kv;
+    const bool is_new = kNew && p == nr.page && r == nr.slot;
+    const int cv = slot ^ PT::vswz(r);
+    const uint16_t* src = ok ? (is_new ? nr.v + cv * 8 : a.v_pool + blk + r * D + cv * 8) : zero;
+    lds_dma16_untracked<true>(src, dst + PT::TBYTES + i * 1024);
   }
 }
 
+// Attends the G heads to logical page p staged at buf, updating the wave's online softmax state.
 template <int D>
-__device__ __forceinline__ void decode_consume(const AttnArgs& a, const DecodeK<D>& K, int pa, bool pb_ok,
-                                               int kv, const bf16x8* qop, f32x4* oacc, float& m_run,
-                                               float& l_run, const char* vbuf) {
-  using VT = VTile<D>;
-  constexpr int KB = DecodeK<D>::KB;
-  constexpr int MB = D / 16;                       // 16-wide dim blocks of the PV product
-  const int lane = threadIdx.x & 63, gi = lane >> 4;
-  const float c = a.scale_log2;
-  const int pb = pa + 1;
-  f32x4 sa = f32x4{0.f, 0.f, 0.f, 0.f}, sb = f32x4{0.f, 0.f, 0.f, 0.f};
+__device__ __forceinline__ void decode_consume(int p, int kv, const bf16x8* qop, f32x4* oacc, float& m_run,
+                                               float& l_run, const float c, const char* buf) {
+  using PT = PageTile<D>;
+  const int lane = threadIdx.x & 63, gi = lane >> 4, j = lane & 15;
+  // S^T: lane l holds head l % 16 of keys 4 gi .. 4 gi + 3; its K operand is row l % 16, dims of
+  // chunk 4 kb + gi (the Q operand holds the same dims)
+  f32x4 sc = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int kb = 0; kb < KB; ++kb) {
-    sa = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(K.ka[kb]), qop[kb], sa, 0, 0, 0);
-    sb = __builtin_amdgcn_mfma_f32_16x16x32_bf16(as_bf16x8(K.kb[kb]), qop[kb], sb, 0, 0, 0);
+  for (int kb = 0; kb < PT::KB; ++kb) {
+    const bf16x8 kop = *reinterpret_cast<const bf16x8*>(buf + PT::koff(j, 4 * kb + gi));
+    sc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kop, qop[kb], sc, 0, 0, 0);
   }
-  // mask keys past the end of the sequence / split (a select, so stray bit patterns never leak)
+  // mask keys past the end of the sequence (a select, so stray bit patterns never leak)
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    sa[r] = (pa * kPage + 4 * gi + r < kv) ? sa[r] : -INFINITY;
-    sb[r] = (pb_ok && pb * kPage + 4 * gi + r < kv) ? sb[r] : -INFINITY;
-  }
-  float mx = fmaxf(fmaxf(fmaxf(sa[0], sa[1]), fmaxf(sa[2], sa[3])), fmaxf(fmaxf(sb[0], sb[1]), fmaxf(sb[2], sb[3])));
+  for (int r = 0; r < 4; ++r) sc[r] = (p * kPage + 4 * gi + r < kv) ? sc[r] : -INFINITY;
+  float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
   mx = fmaxf(mx, __shfl_xor(mx, 16));
   mx = fmaxf(mx, __shfl_xor(mx, 32));
-  // the maximum only moves when this page pair exceeds it, and the O rescale is skipped when no
-  // lane of the wave moved (decode is bound by HBM, so it keeps the exact maximum)
+  // the maximum only moves when this page exceeds it, and the O rescale is skipped when no lane
+  // of the wave moved (decode is bound by HBM, so it keeps the exact maximum)
   const bool grow = mx * c > m_run;
   const float m_new = grow ? mx * c : m_run;
   const float alpha = grow ? fexp2(m_run - m_new) : 1.0f;
-  bf16x8 pop;
+  i16x4 pop;
   float psum = 0.f;
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const float p0 = fexp2(__builtin_fmaf(sa[r], c, -m_new));
-    const float p1 = fexp2(__builtin_fmaf(sb[r], c, -m_new));
-    psum += p0 + p1;
-    pop[r] = (__bf16)p0;
-    pop[4 + r] = (__bf16)p1;
+    const float pr = fexp2(__builtin_fmaf(sc[r], c, -m_new));
+    psum += pr;
+    pop[r] = (short)bf16_bits(pr);
   }
   l_run = l_run * alpha + psum;
   if (__ballot(grow)) {
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) oacc[mb] *= alpha;
+    for (int mb = 0; mb < PT::MB; ++mb) oacc[mb] *= alpha;
   }
   m_run = m_new;
-  {
-    const int j = lane & 15;
-    const int r0 = 4 * gi + (j >> 2);              // rows of page a; page b rows are +16
+  // O^T += V^T P^T: the transposing read gives lane l dim 16 mb + l % 16 of keys 4 gi .. 4 gi + 3,
+  // the k index of the P^T operand that lane already holds
+  const int r0 = 4 * gi + (j >> 2);
 #pragma unroll
-    for (int mb = 0; mb < MB; ++mb) {
-      const int d0 = 16 * mb + 4 * (j & 3);
-      const i16x4 v0 = lds_read_tr(vbuf, VT::off(r0, d0));
-      const i16x4 v1 = lds_read_tr(vbuf, VT::off(r0 + kPage, d0));
-      oacc[mb] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(concat_tr(v0, v1), pop, oacc[mb], 0, 0, 0);
-    }
+  for (int mb = 0; mb < PT::MB; ++mb) {
+    const i16x4 v = lds_read_tr(buf, PT::voff(r0, 16 * mb + 4 * (j & 3)));
+    oacc[mb] = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(v, pop, oacc[mb], 0, 0, 0);
   }
 }
 
 
-// Page ids of the pair a wave will issue next, read with scalar loads from the block table.
-struct PairPages {
-  int phys_a, phys_b, pa;
-  bool pb_ok;
-};
-
-
-__device__ __forceinline__ PairPages pair_pages(ConstI32Ptr bt_row, int p_begin, int p_end, int pi, int num_pages) {
-  PairPages pp;
-  pp.pa = p_begin + 2 * pi;
-  pp.pb_ok = pp.pa + 1 < p_end;
-  pp.phys_a = clamp_page(bt_row[pp.pa], num_pages);
-  // a missing second page re-reads the first (index stays inside the row)
-  pp.phys_b = pp.pb_ok ? clamp_page(bt_row[pp.pa + 1], num_pages) : pp.phys_a;
-  return pp;
+// Physical page of logical page p of the row, read with a scalar load from the block table.
+__device__ __forceinline__ int page_id(ConstI32Ptr bt_row, int p, int num_pages) {
+  return clamp_page(bt_row[p], num_pages);
 }
 
 // One decode work item as the kernels see it: sequence b (its new token is row q_row of q/out),
@@ -1151,21 +1148,23 @@ __device__ __forceinline__ int count_split_in(const AttnArgs& a, const DecItem& 
   return prev == it.n_splits - 1;
 }
 
-// One pipeline step: issue the next pair (K into k_next, V by DMA into v_next), then consume the
-// current pair from k_cur / v_cur.  The step is branch-free: a wave with no further pair re-issues
-// its current pair (L2 hits, results unused), so every step leaves exactly one pair in flight.
-// The two V buffers are __restrict__ parameters of this one function, so the compiler knows the
-// reads of v_cur cannot alias the DMA still writing v_next and waits only for the current pair.
+// One pipeline step: issue the next page's copies into s_next, then wait for the current page's
+// and consume it from s_cur.  The step is branch-free: a wave with no further page re-issues its
+// current page (cache hits, results unused), so every step leaves exactly one page in flight.
+// The copies are issued untracked, so the compiler adds no waits of its own for them (left to
+// itself it drained every copy in flight in one of the loop's two unrolled steps); s_next was last
+// read in the previous step, whose operand reads all completed before its MFMAs.
 template <int D, bool kNew>
-__device__ __forceinline__ void decode_step(const AttnArgs& a, const PairPages& cur, const PairPages& nxt, int g,
-                                            int kv, DecodeK<D>& k_next, const DecodeK<D>& k_cur,
-                                            char* __restrict__ v_next, const char* __restrict__ v_cur,
+__device__ __forceinline__ void decode_step(const AttnArgs& a, int p_cur, int p_nxt, int phys_nxt, int g, int kv,
+                                            char* __restrict__ s_next, const char* __restrict__ s_cur,
                                             const bf16x8* qop, f32x4* oacc, float& m_run, float& l_run,
                                             const NewRow& nr) {
-  constexpr int PAIR_LOADS = 2 * DecodeK<D>::KB + VTile<D>::NDMA;   // vector-memory ops per pair
-  decode_issue<D, kNew>(a, nxt.phys_a, nxt.phys_b, nxt.pb_ok, nxt.pa, g, kv, k_next, v_next, nr);
-  __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(PAIR_LOADS));              // the current pair has landed
-  decode_consume<D>(a, k_cur, cur.pa, cur.pb_ok, kv, qop, oacc, m_run, l_run, v_cur);
+  constexpr int PAGE_LOADS = 2 * PageTile<D>::NDMA;   // vector-memory ops per page
+  decode_issue<D, kNew>(a, phys_nxt, p_nxt, g, kv, s_next, nr);
+  // the current page has landed; the copies are invisible to the compiler, so the wait is also a
+  // compiler barrier that keeps the stage reads below it
+  __asm__ volatile("s_waitcnt vmcnt(%0)" ::"n"(PAGE_LOADS) : "memory");
+  decode_consume<D>(p_cur, kv, qop, oacc, m_run, l_run, a.scale_log2, s_cur);
 }
 
 // kMergeHere: a multi-split (sequence, kv-head) is merged inside the attention kernel by the split
@@ -1176,13 +1175,12 @@ __device__ __forceinline__ void decode_step(const AttnArgs& a, const PairPages& 
 // before_end: called by every thread just before the item's closing barrier (decode_kernel
 // decodes its next item there, so the claim's latency hides behind this item).
 template <int D, int NW, bool kMergeHere, typename BeforeEnd>
-__device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& it, int pps, char* vbufA,
-                                             char* vbufB, DecItem& pend, int* s_flag, BeforeEnd before_end) {
+__device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& it, int pps, char* stageA,
+                                             char* stageB, DecItem& pend, int* s_flag, BeforeEnd before_end) {
   constexpr int NT = NW * 64;
-  using VT = VTile<D>;
-  constexpr int MB = D / 16;
-  constexpr int KB = DecodeK<D>::KB;
-  constexpr int PAIR_LOADS = 2 * KB + VT::NDMA;    // vector-memory instructions issued per pair
+  using PT = PageTile<D>;
+  constexpr int MB = PT::MB;
+  constexpr int KB = PT::KB;
   const int lane = threadIdx.x & 63, w = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);   // wave index (uniform)
   const int gi = lane >> 4, hh = lane & 15;
   const int b = it.b, split = it.split, g = it.g;
@@ -1191,10 +1189,10 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& i
   const int n_pages = (kv + kPage - 1) / kPage;
   const int p_begin = split * pps;
   const int p_end = min(p_begin + pps, n_pages);
-  const int n_pairs = (p_end - p_begin + 1) / 2;
+  const int n_pg = p_end - p_begin;                 // pages of this split (>= 1)
   const bool head_ok = hh < G;
-  char* vb0 = vbufA + w * VT::PAIR_BYTES;
-  char* vb1 = vbufB + w * VT::PAIR_BYTES;
+  char* st0 = stageA + w * PT::BYTES;
+  char* st1 = stageB + w * PT::BYTES;
 
   const ConstI32Ptr bt_row = (ConstI32Ptr)(a.block_table + (size_t)b * a.bt_stride);
 
@@ -1207,9 +1205,9 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& i
       qop[kb] = head_ok ? v : zero_bf16x8();
     }
   }
-  DecodeK<D> kA, kB;
-  const int last = n_pairs - 1;
-  PairPages cur = pair_pages(bt_row, p_begin, p_end, min(w, last), a.num_pages);
+  // the page ids run one page ahead of the copies, which run one page ahead of the compute
+  int cur = min(w, n_pg - 1);
+  int ph_cur = page_id(bt_row, p_begin + cur, a.num_pages);
   // fused append (decode kernel with k_new): the split holding the sequence's last page takes the
   // new token's K/V from k_new / v_new; its last wave writes them into the pools once the item's
   // reads are done (a write whose page id is out of range is skipped, as pearl_kv_append does).
@@ -1221,25 +1219,30 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& i
       nr = NewRow{(kv - 1) / kPage, (kv - 1) % kPage, a.k_new + row, a.v_new + row};
     }
   }
-  if (w < n_pairs) decode_issue<D, kMergeHere>(a, cur.phys_a, cur.phys_b, cur.pb_ok, cur.pa, g, kv, kA, vb0, nr);
+  if (w < n_pg) decode_issue<D, kMergeHere>(a, ph_cur, p_begin + cur, g, kv, st0, nr);
   f32x4 oacc[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) oacc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  // page ids run one pair ahead of the loads, which run one pair ahead of the compute
-  PairPages nxt = w + NW < n_pairs ? pair_pages(bt_row, p_begin, p_end, w + NW, a.num_pages) : cur;
-  for (int pi = w; pi < n_pairs; pi += 2 * NW) {
-    const int pj = pi + NW, pk = pj + NW;
-    const PairPages n2 = pk < n_pairs ? pair_pages(bt_row, p_begin, p_end, pk, a.num_pages) : nxt;
-    decode_step<D, kMergeHere>(a, cur, nxt, g, kv, kB, kA, vb1, vb0, qop, oacc, m_run, l_run, nr);
-    if (pj >= n_pairs) break;
-    const PairPages n3 = pk + NW < n_pairs ? pair_pages(bt_row, p_begin, p_end, pk + NW, a.num_pages) : n2;
-    decode_step<D, kMergeHere>(a, nxt, n2, g, kv, kA, kB, vb0, vb1, qop, oacc, m_run, l_run, nr);
+  int nxt = min(w + NW, n_pg - 1);                 // past the last page: the current one again
+  int ph_nxt = page_id(bt_row, p_begin + nxt, a.num_pages);
+  for (int pi = w; pi < n_pg; pi += 2 * NW) {
+    const int pj = pi + NW;
+    const int n2 = min(pj + NW, n_pg - 1);
+    const int ph_n2 = page_id(bt_row, p_begin + n2, a.num_pages);
+    decode_step<D, kMergeHere>(a, p_begin + cur, p_begin + nxt, ph_nxt, g, kv, st1, st0, qop, oacc, m_run,
+                               l_run, nr);
+    if (pj >= n_pg) break;
+    const int n3 = min(pj + 2 * NW, n_pg - 1);
+    const int ph_n3 = page_id(bt_row, p_begin + n3, a.num_pages);
+    decode_step<D, kMergeHere>(a, p_begin + nxt, p_begin + n2, ph_n2, g, kv, st0, st1, qop, oacc, m_run,
+                               l_run, nr);
     cur = n2;
     nxt = n3;
+    ph_nxt = ph_n3;
   }
-  __builtin_amdgcn_s_waitcnt(PEARL_VMCNT(0));      // drain the trailing re-issued pair
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");   // drain the trailing re-issued page
   // the new row's bytes and page id are loaded now, to be stored once the LDS merge below has
   // waited for them
   const bool writer = kMergeHere && nr.page >= 0 && w == NW - 1 && lane < D / 8;
@@ -1256,8 +1259,8 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& i
 
   // merge the waves' states through LDS
   __syncthreads();
-  static_assert(Lds<D, NW, 2>::merge_bytes <= NW * VT::PAIR_BYTES, "merge scratch fits in a V buffer");
-  float* mo = reinterpret_cast<float*>(vbufA);                // [wave][8 heads][D]
+  static_assert(Lds<D, NW, 2>::merge_bytes <= NW * PT::BYTES, "merge scratch fits in one set of stages");
+  float* mo = reinterpret_cast<float*>(stageA);               // [wave][8 heads][D]
   float* mm = mo + NW * 8 * D;                            // [wave][8]
   float* ml = mm + NW * 8;                                // [wave][8]
   if (head_ok) {
@@ -1343,12 +1346,12 @@ template <int D, int kKinds>
 __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnArgs a, int max_pre) {
   constexpr int NW = KernelCfg<D, kKinds>::NW;
   __shared__ __attribute__((aligned(16))) char smem[Lds<D, NW, kKinds>::bytes];
-  // the two V buffers of the decode pipeline are separate objects so the LDS reads of one are
+  // the two stages of the decode pipeline are separate objects so the LDS reads of one are
   // known not to alias the LDS-DMA writes still in flight into the other
-  __shared__ __attribute__((aligned(16))) char vbufA_[(kKinds == 2) ? NW * VTile<D>::PAIR_BYTES : 16];
-  __shared__ __attribute__((aligned(16))) char vbufB_[(kKinds == 2) ? NW * VTile<D>::PAIR_BYTES : 16];
-  char* vbufA = (kKinds == 2) ? vbufA_ : smem;
-  char* vbufB = (kKinds == 2) ? vbufB_ : smem + NW * VTile<D>::PAIR_BYTES;
+  __shared__ __attribute__((aligned(16))) char stageA_[(kKinds == 2) ? NW * PageTile<D>::BYTES : 16];
+  __shared__ __attribute__((aligned(16))) char stageB_[(kKinds == 2) ? NW * PageTile<D>::BYTES : 16];
+  char* stageA = (kKinds == 2) ? stageA_ : smem;
+  char* stageB = (kKinds == 2) ? stageB_ : smem + NW * PageTile<D>::BYTES;
   // prefill-only kernels: three K and three V stage buffers, each set contiguous
   constexpr int kDT = (kKinds == 1) ? DmaTile<D>::BYTES : 16;
   __shared__ __attribute__((aligned(16))) char pk[3 * kDT], pv[3 * kDT];
@@ -1413,7 +1416,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
         if constexpr (kKinds == 1) {
           prefill_tile_pp<D>(a, e, en.x, en.y, g, split_keys, pk, pv);
         } else {
-          // the mixed kernel's stage buffers share its LDS region with the decode V buffers (a
+          // the mixed kernel's prefill stage buffers share its LDS region with the decode stages (a
           // workgroup runs one item at a time, and items are separated by a drained barrier)
           constexpr int B = DmaTile<D>::BYTES;
           static_assert(6 * B <= Lds<D, NW, kKinds>::bytes, "stage buffers fit the shared region");
@@ -1426,7 +1429,7 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
         const SeqInfo si = a.seqinfo[en.x];
         const DecItem it{en.x, en.y, g, si.q_start, si.ctx_len + si.q_len, si.kind >> 4, a.split_base[en.x]};
         DecItem none{-1, 0, 0, 0, 0, 0, 0};
-        decode_split<D, NW, false>(a, it, pps, vbufA, vbufB, none, nullptr, [] {});
+        decode_split<D, NW, false>(a, it, pps, stageA, stageB, none, nullptr, [] {});
       }
     }
     __syncthreads();
@@ -1633,8 +1636,8 @@ template <int D>
 __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a, DecPlanArgs d) {
   constexpr int NW = kWaves;
   // separate objects, so the LDS reads of one are known not to alias the LDS-DMA into the other
-  __shared__ __attribute__((aligned(16))) char vbufA[NW * VTile<D>::PAIR_BYTES];
-  __shared__ __attribute__((aligned(16))) char vbufB[NW * VTile<D>::PAIR_BYTES];
+  __shared__ __attribute__((aligned(16))) char stageA[NW * PageTile<D>::BYTES];
+  __shared__ __attribute__((aligned(16))) char stageB[NW * PageTile<D>::BYTES];
   __shared__ DecPlanLds P;
   __shared__ DecItem s_it[2];
   __shared__ int s_flag;
@@ -1654,7 +1657,7 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a, DecPlanArg
     const DecItem it = s_it[slot];
     int nx = 0;
     if (threadIdx.x == 0) nx = atomicAdd(&a.ws_hdr[kHdrCounter], 1);   // used at the item's end
-    decode_split<D, NW, true>(a, it, pps, vbufA, vbufB, pend, &s_flag, [&] {
+    decode_split<D, NW, true>(a, it, pps, stageA, stageB, pend, &s_flag, [&] {
       if (threadIdx.x == 0) s_it[slot ^ 1] = nx < n_items ? decode_item(P, nx, H, B) : none;
     });                                             // ends with a barrier
     slot ^= 1;
