@@ -333,16 +333,21 @@ def hbm_probe(torch, nbytes=1 << 30, reps=10):
         t = [a.elapsed_time(b) for a, b in ev]
         return float(np.median(t)), float(min(t))
     t_read = timed(lambda: bd.hbm_read(src, sink))
+    t_read_nt = timed(lambda: bd.hbm_read(src, sink, nontemporal=True))
     t_write = timed(lambda: bd.hbm_fill(dst, 0x11111111))
     t_copy = timed(lambda: bd.hbm_copy(src, dst))
     gbps = lambda moved, t: round(moved / (t * 1e-3) / 1e9, 1)
-    fig = {"bytes": nbytes, "what": "library streaming kernels (pearl_hbm_read / _fill / _copy), 16-byte "
-                                    "vectors, median of %d launches each after a 1 GiB read flush; the "
-                                    "write and copy figures exclude write-back still pending in the "
-                                    "caches when the kernel ends" % reps,
-           "read_GBps": gbps(nbytes, t_read[0]), "write_GBps": gbps(nbytes, t_write[0]),
-           "copy_GBps": gbps(2 * nbytes, t_copy[0]),
-           "read_GBps_best": gbps(nbytes, t_read[1]), "copy_GBps_best": gbps(2 * nbytes, t_copy[1])}
+    fig = {"bytes": nbytes, "what": "library streaming kernels (pearl_hbm_read / _read_nt / _fill / _copy), "
+                                    "16-byte vectors, median of %d launches each after a 1 GiB read flush; "
+                                    "read_nt and copy mark their loads non-temporal, the faster read mode; "
+                                    "the write and copy figures exclude write-back still pending in the "
+                                    "caches when the kernel ends; frac_of_measured.read is against the "
+                                    "faster of the two read figures" % reps,
+           "read_GBps": gbps(nbytes, t_read[0]), "read_nt_GBps": gbps(nbytes, t_read_nt[0]),
+           "write_GBps": gbps(nbytes, t_write[0]), "copy_GBps": gbps(2 * nbytes, t_copy[0]),
+           "read_GBps_best": gbps(nbytes, t_read[1]), "read_nt_GBps_best": gbps(nbytes, t_read_nt[1]),
+           "copy_GBps_best": gbps(2 * nbytes, t_copy[1])}
+    fig["read_best_mode_GBps"] = max(fig["read_GBps"], fig["read_nt_GBps"])
     del src, dst
     return fig, flush, (scratch, sink)
 
@@ -882,11 +887,11 @@ def main():
 
     probe, flush, _flush_buf = hbm_probe(torch)
     torch.cuda.empty_cache()
-    log("bench: measured HBM: read %.0f GB/s, write %.0f GB/s, copy %.0f GB/s"
-        % (probe["read_GBps"], probe["write_GBps"], probe["copy_GBps"]))
+    log("bench: measured HBM: read %.0f GB/s (non-temporal %.0f), write %.0f GB/s, copy %.0f GB/s"
+        % (probe["read_GBps"], probe["read_nt_GBps"], probe["write_GBps"], probe["copy_GBps"]))
 
     def vs_measured(gbps):
-        return {"read": round(gbps / probe["read_GBps"], 4), "copy": round(gbps / probe["copy_GBps"], 4)}
+        return {"read": round(gbps / probe["read_best_mode_GBps"], 4), "copy": round(gbps / probe["copy_GBps"], 4)}
 
     # ---- headline: Qwen3-8B decode, B=64 -------------------------------------------------------
     log("bench: generating qwen3-8b decode (B=64, ctx U[2048,16384])")
@@ -1024,7 +1029,7 @@ def main():
                 entry["roofline_ms_overlapped"] = round(max(t_hbm, t_mfma), 4)
                 entry["roofline_ms_serial"] = round(t_hbm + t_mfma, 4)
                 entry["frac_of_overlapped_bound"] = round(max(t_hbm, t_mfma) / ms_k, 4)
-                t_hbm_m = b_ / (probe["read_GBps"] * 1e9) * 1e3
+                t_hbm_m = b_ / (probe["read_best_mode_GBps"] * 1e9) * 1e3
                 entry["frac_of_overlapped_bound_measured_hbm"] = round(max(t_hbm_m, t_mfma) / ms_k, 4)
             log("bench:   %s" % json.dumps(entry))
             sec.append(entry)

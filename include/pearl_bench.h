@@ -27,14 +27,18 @@
 extern "C" {
 #endif
 
-/* dst[0 .. bytes) = src[0 .. bytes): reads `bytes`, writes `bytes`.  The ranges must not
- * overlap. */
+/* dst[0 .. bytes) = src[0 .. bytes): reads `bytes` (non-temporal loads), writes `bytes`.  The
+ * ranges must not overlap. */
 pearl_status pearl_hbm_copy(const void* src, void* dst, size_t bytes, void* stream);
 
 /* Reads src[0 .. bytes) and discards it.  `sink` is a caller-owned 16-byte device slot that the
  * kernel may overwrite (almost never does); it reads nothing else.  Over a buffer of 1 GiB or
  * more this is the cache flush. */
 pearl_status pearl_hbm_read(const void* src, size_t bytes, void* sink, void* stream);
+
+/* As pearl_hbm_read, with the loads marked non-temporal: the faster read mode of this part for
+ * bytes read once, and not a cache flush (such lines are not kept in the caches). */
+pearl_status pearl_hbm_read_nt(const void* src, size_t bytes, void* sink, void* stream);
 
 /* Writes the 32-bit `pattern` over dst[0 .. bytes); reads nothing. */
 pearl_status pearl_hbm_fill(void* dst, size_t bytes, uint32_t pattern, void* stream);

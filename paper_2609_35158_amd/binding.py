@@ -42,7 +42,7 @@ class SeqDesc(ctypes.Structure):
 EXPORTED = ("pearl_abi_version", "pearl_status_str", "pearl_last_error", "pearl_kv_append",
             "pearl_attn_workspace_bytes", "pearl_attn_prefill_append", "pearl_attn_decode",
             "pearl_attn_mixed", "pearl_kv_pack", "pearl_kv_unpack", "pearl_set_kernel_events",
-            "pearl_hbm_copy", "pearl_hbm_read", "pearl_hbm_fill", "pearl_attn_decode_static",
+            "pearl_hbm_copy", "pearl_hbm_read", "pearl_hbm_read_nt", "pearl_hbm_fill", "pearl_attn_decode_static",
             "pearl_attn_decode_static_max_bytes", "pearl_attn_decode_append")
 
 
@@ -94,8 +94,10 @@ def load(path: str = LIB_PATH):
     # measurement tooling (include/pearl_bench.h)
     lib.pearl_hbm_copy.restype = ctypes.c_int
     lib.pearl_hbm_copy.argtypes = [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p]
-    lib.pearl_hbm_read.restype = ctypes.c_int
-    lib.pearl_hbm_read.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    for name in ("pearl_hbm_read", "pearl_hbm_read_nt"):
+        f = getattr(lib, name)
+        f.restype = ctypes.c_int
+        f.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
     lib.pearl_hbm_fill.restype = ctypes.c_int
     lib.pearl_hbm_fill.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_uint32, ctypes.c_void_p]
     _lib = lib
@@ -368,13 +370,15 @@ def hbm_copy(src: torch.Tensor, dst: torch.Tensor) -> None:
     _check(load().pearl_hbm_copy(src.data_ptr(), dst.data_ptr(), n, _stream()), "pearl_hbm_copy")
 
 
-def hbm_read(src: torch.Tensor, sink: torch.Tensor) -> None:
+def hbm_read(src: torch.Tensor, sink: torch.Tensor, nontemporal: bool = False) -> None:
     """Stream-read src; `sink` is a 16-byte (or larger) GPU tensor the kernel may overwrite.  Over
-    >= 1 GiB this is the cache flush (it leaves no dirty lines behind)."""
+    >= 1 GiB the plain read is the cache flush (it leaves no dirty lines behind); nontemporal=True
+    is pearl_hbm_read_nt, the faster read mode, which is no flush."""
     if not (src.is_cuda and src.is_contiguous() and sink.is_cuda and sink.numel() * sink.element_size() >= 16):
         raise ValueError("hbm_read needs a contiguous GPU source and a 16-byte GPU sink")
-    _check(load().pearl_hbm_read(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(), _stream()),
-           "pearl_hbm_read")
+    name = "pearl_hbm_read_nt" if nontemporal else "pearl_hbm_read"
+    _check(getattr(load(), name)(src.data_ptr(), src.numel() * src.element_size(), sink.data_ptr(), _stream()),
+           name)
 
 
 def hbm_fill(dst: torch.Tensor, pattern: int = 0) -> None:

@@ -7,7 +7,10 @@
 //
 // Each workgroup streams one contiguous span of kSpan 16-byte vectors; thread t handles vectors
 // t, t + 256, ..., so every load and store instruction of a wave covers 1 KiB of consecutive
-// bytes, and all kUnroll loads of a thread are in flight before its first store.
+// bytes, and all kUnroll loads of a thread are in flight before its first store.  The copy and
+// the second read mode mark their loads non-temporal (read once, not kept in the caches), which
+// on this part reads faster than plain loads (1 GiB: about 6.1 against 5.7 TB/s copied); the
+// plain read mode is the cache flush, since it leaves the caches full of its own clean lines.
 
 #include "pearl_internal.h"
 #include "../../include/pearl_bench.h"
@@ -20,7 +23,13 @@ constexpr int kProbeThreads = 256;
 constexpr int kProbeUnroll = 8;
 constexpr size_t kSpan = (size_t)kProbeThreads * kProbeUnroll;   // vectors per workgroup
 
-enum ProbeMode : int { kProbeCopy = 0, kProbeRead = 1, kProbeFill = 2 };
+enum ProbeMode : int { kProbeCopy = 0, kProbeRead = 1, kProbeFill = 2, kProbeReadOnce = 3 };
+
+template <int kMode>
+__device__ __forceinline__ v4u probe_load(const v4u* p) {
+  if constexpr (kMode == kProbeRead) return *p;
+  else return __builtin_nontemporal_load(p);
+}
 
 template <int kMode>
 __global__ __launch_bounds__(kProbeThreads) void hbm_stream_kernel(const v4u* __restrict__ src,
@@ -39,7 +48,7 @@ __global__ __launch_bounds__(kProbeThreads) void hbm_stream_kernel(const v4u* __
 #pragma unroll
   for (int u = 0; u < kProbeUnroll; ++u) {
     const size_t i = base + (size_t)u * kProbeThreads;
-    x[u] = i < n ? src[i] : v4u{0u, 0u, 0u, 0u};
+    x[u] = i < n ? probe_load<kMode>(src + i) : v4u{0u, 0u, 0u, 0u};
   }
   if (kMode == kProbeCopy) {
 #pragma unroll
@@ -80,6 +89,8 @@ pearl_status launch_probe(int mode, const void* src, void* dst, size_t bytes, ui
     hipLaunchKernelGGL(hbm_stream_kernel<kProbeCopy>, grid, block, 0, s, in, out, n, key);
   else if (mode == kProbeRead)
     hipLaunchKernelGGL(hbm_stream_kernel<kProbeRead>, grid, block, 0, s, in, out, n, key);
+  else if (mode == kProbeReadOnce)
+    hipLaunchKernelGGL(hbm_stream_kernel<kProbeReadOnce>, grid, block, 0, s, in, out, n, key);
   else
     hipLaunchKernelGGL(hbm_stream_kernel<kProbeFill>, grid, block, 0, s, in, out, n, key);
   const hipError_t e = hipGetLastError();
@@ -99,6 +110,10 @@ pearl_status pearl_hbm_copy(const void* src, void* dst, size_t bytes, void* stre
 pearl_status pearl_hbm_read(const void* src, size_t bytes, void* sink, void* stream) {
   // the key is a value a fold of real data essentially never takes; a match only writes the sink
   return pearl::launch_probe(pearl::kProbeRead, src, sink, bytes, 0x9e3779b9u, stream, "pearl_hbm_read");
+}
+
+pearl_status pearl_hbm_read_nt(const void* src, size_t bytes, void* sink, void* stream) {
+  return pearl::launch_probe(pearl::kProbeReadOnce, src, sink, bytes, 0x9e3779b9u, stream, "pearl_hbm_read_nt");
 }
 
 pearl_status pearl_hbm_fill(void* dst, size_t bytes, uint32_t pattern, void* stream) {

@@ -70,7 +70,10 @@ __global__ __launch_bounds__(kCopyThreads) void kv_copy_kernel(
         x[u] = ok[u] ? rows[roff] : u32x4{0u, 0u, 0u, 0u};
         dst[u] = poff;
       } else {
-        x[u] = ok[u] && page_ok ? pool[poff] : u32x4{0u, 0u, 0u, 0u};
+        // pool pages are read once here: a non-temporal load (measured 5.12 -> 5.48 TB/s on a
+        // 2.47 GB pack; rows -> pool copies measured no gain from it, and non-temporal stores
+        // were slower in every direction)
+        x[u] = ok[u] && page_ok ? __builtin_nontemporal_load(&pool[poff]) : u32x4{0u, 0u, 0u, 0u};
         dst[u] = roff;
       }
     }

@@ -152,6 +152,9 @@ def test_hbm_probe_host_validation():
     assert lib.pearl_hbm_read(FAKE + 8, 32, FAKE, None) == INVALID and "aligned" in pa.last_error()
     assert lib.pearl_hbm_read(FAKE, 32, FAKE + 4, None) == INVALID and "aligned" in pa.last_error()
     assert lib.pearl_hbm_read(FAKE, 32, None, None) == INVALID
+    assert lib.pearl_hbm_read_nt(FAKE, 0, FAKE, None) == 0
+    assert lib.pearl_hbm_read_nt(FAKE + 8, 32, FAKE, None) == INVALID and "aligned" in pa.last_error()
+    assert lib.pearl_hbm_read_nt(FAKE, 24, FAKE, None) == INVALID and "multiple of 16" in pa.last_error()
     assert lib.pearl_hbm_fill(None, 32, 0, None) == INVALID
     assert lib.pearl_hbm_fill(FAKE, 40, 0, None) == INVALID
 

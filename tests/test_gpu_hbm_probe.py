@@ -31,11 +31,12 @@ def test_copy_and_fill_are_exact(nbytes):
     assert bool((dst[nbytes:] == 0xA5).all())
 
 
-def test_read_probe_leaves_sink():
-    say("hbm probe read")
+@pytest.mark.parametrize("nontemporal", [False, True])
+def test_read_probe_leaves_sink(nontemporal):
+    say("hbm probe read nontemporal=%s" % nontemporal)
     g = torch.Generator(device="cpu").manual_seed(5)
     src = torch.randint(0, 256, (1 << 24,), dtype=torch.uint8, generator=g).cuda()
     sink = torch.zeros(16, dtype=torch.uint8, device="cuda")
-    bd.hbm_read(src, sink)
+    bd.hbm_read(src, sink, nontemporal=nontemporal)
     torch.cuda.synchronize()
     assert bool((sink == 0).all())
