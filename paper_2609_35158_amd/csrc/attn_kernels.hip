@@ -223,7 +223,7 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
   __syncthreads();
   if (s_err) {
     if (tid == 0) {
-      hdr[kHdrCounter] = 0; hdr[kHdrCounterPre] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
+      hdr[kHdrCounter] = 0; hdr[kHdrNumPre] = 0; hdr[kHdrNumDec] = 0;
       hdr[kHdrError] = 1; hdr[kHdrNumItems] = 0; hdr[kHdrPreSplitKeys] = 0; hdr[kHdrNumPreJobs] = 0;
       hdr[kHdrPagesPerSplit] = p.pages_per_split;
     }
@@ -416,7 +416,6 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     const bool over = n_pre > p.max_pre || n_dec > p.max_dec || n_jobs > p.pre_jobs_cap ||
                       (n_jobs > 0 && (long long)n_pre * p.num_kv_heads > p.pre_slots);
     hdr[kHdrCounter] = 0;
-    hdr[kHdrCounterPre] = 0;
     hdr[kHdrPreFirstWG] = s_pre_first;
     hdr[kHdrNumPre] = over ? 0 : n_pre;
     hdr[kHdrNumDec] = over ? 0 : n_dec;
@@ -1361,43 +1360,47 @@ __global__ __launch_bounds__((KernelCfg<D, kKinds>::NT)) void attn_kernel(AttnAr
   const int split_keys = a.ws_hdr[kHdrPreSplitKeys];
   const int pps = a.ws_hdr[kHdrPagesPerSplit];
   const int H_kv = a.num_kv_heads;
-  // Items: prefill items [0, n_pre * H_kv), decode items after them.  Prefill-only and
-  // decode-only launches hand them out with one counter.  Mixed launches keep a counter per kind;
-  // workgroups below kHdrPreFirstWG take prefill items first, the others decode items first, and
-  // each takes the other kind once its own is exhausted, so both kinds run side by side.
+  // Items: prefill items [0, n_pre * H_kv), decode items after them.  Prefill items are handed
+  // out by the per-XCD queues below, decode items by one counter.  In mixed launches workgroups
+  // below kHdrPreFirstWG take prefill items first, the others decode items first, and each takes
+  // the other kind once its own is exhausted, so both kinds run side by side.
   const int n_pre_items = n_pre * H_kv;
   const bool pre_first = (int)blockIdx.x < a.ws_hdr[kHdrPreFirstWG];
-  // Prefill-only launches: item i belongs to queue i % 8, and a workgroup takes the items of the
-  // queue of the XCD it runs on, then those of the other queues in turn.  With 8 kv-heads (or a
-  // multiple or divisor of 8) the items of one (sequence, kv-head) then share one XCD's L2: every
-  // tile of a sequence re-reads that head's whole context, which other XCDs would each fetch
-  // from memory again.  The queues are balanced (the 8 heads of a tile are equal work), and the
-  // turn to other queues completes every item wherever the workgroups run.
+  // Prefill items: item i belongs to queue i % 8, and a workgroup takes the items of the queue of
+  // the XCD it runs on, then those of the other queues in turn.  With 8 kv-heads the items of
+  // one (sequence, kv-head) then share one XCD's L2 (with 4, two XCDs): every tile of a sequence
+  // re-reads that head's whole context, which other XCDs would each fetch from memory again.  The
+  // queues are balanced (the heads of a tile are equal work), and the turn to other queues
+  // completes every item wherever the workgroups run.
   int queue = xcc_id(), queues_left = kNumXcd;      // thread 0's claim state
+  auto claim_pre = [&](int limit) -> int {          // a prefill item below limit, or -1
+    while (queues_left > 0) {
+      const int c = atomicAdd(&a.ws_hdr[kHdrQueues + queue], 1);
+      const int64_t i = queue + (int64_t)kNumXcd * c;
+      if (i < limit) return (int)i;
+      queue = (queue + 1) % kNumXcd;
+      --queues_left;
+    }
+    return -1;
+  };
   auto claim = [&]() -> int {
     if constexpr (kKinds == 1) {
-      while (queues_left > 0) {
-        const int c = atomicAdd(&a.ws_hdr[kHdrQueues + queue], 1);
-        const int64_t i = queue + (int64_t)kNumXcd * c;
-        if (i < n_items) return (int)i;
-        queue = (queue + 1) % kNumXcd;
-        --queues_left;
-      }
-      return n_items;
+      const int i = claim_pre(n_items);
+      return i >= 0 ? i : n_items;
     } else if constexpr (kKinds == 2) {
       return atomicAdd(&a.ws_hdr[kHdrCounter], 1);
     } else {
       const int n_dec_items = n_items - n_pre_items;
       if (pre_first) {
-        const int c = atomicAdd(&a.ws_hdr[kHdrCounterPre], 1);
-        if (c < n_pre_items) return c;
+        const int c = claim_pre(n_pre_items);
+        if (c >= 0) return c;
         const int d = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
         return d < n_dec_items ? n_pre_items + d : n_items;
       } else {
         const int d = atomicAdd(&a.ws_hdr[kHdrCounter], 1);
         if (d < n_dec_items) return n_pre_items + d;
-        const int c = atomicAdd(&a.ws_hdr[kHdrCounterPre], 1);
-        return c < n_pre_items ? c : n_items;
+        const int c = claim_pre(n_pre_items);
+        return c >= 0 ? c : n_items;
       }
     }
   };

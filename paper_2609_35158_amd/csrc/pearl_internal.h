@@ -58,10 +58,10 @@ enum Hdr : int {
   kHdrNumItems = 4,    // (pre + dec) * H_kv
   kHdrPreSplitKeys = 5,  // keys per prefill split (a multiple of 64); 0 = tiles are not split
   kHdrNumPreJobs = 6,  // prefill tiles with more than one split (merge jobs)
-  kHdrCounterPre = 7,  // prefill work counter of mixed launches (atomic)
+  // word 7: unused
   kHdrPreFirstWG = 8,  // mixed launches: workgroups [0, this) take prefill items first
   kHdrPagesPerSplit = 9,  // pages per decode split chosen by the planner
-  kHdrQueues = 16,     // words 16..23: prefill-only launches, one work counter per XCD (atomic)
+  kHdrQueues = 16,     // words 16..23: prefill items, one work counter per XCD (atomic)
   kHdrZero = 32,       // words 32..63: a zeroed 128-byte block (source for keys past the end)
   kHdrWords = 64
 };
