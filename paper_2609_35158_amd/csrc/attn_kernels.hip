@@ -243,14 +243,14 @@ __global__ __launch_bounds__(kPlanThreads) void plan_kernel(
     }
     s_split_keys = (int)S;
     // Mixed launches: how many workgroups take prefill items first (the others take decode items
-    // first): 1.35 x prefill's share of the estimated work, in prefill and decode key-units
+    // first): 1.2 x prefill's share of the estimated work, in prefill and decode key-units
     // weighted 3 : 2 as above.  A prefill tile left for the end of a launch holds one workgroup
     // far longer than a decode split, so prefill gets more than its share.
     int pre_first = 0;
     if (p.mixed_grid > 0) {
       const long long pu = 3LL * (long long)s_pre_keys * H;
       const long long du = 2LL * (long long)s_dec_keys * H;
-      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (27LL * p.mixed_grid * pu) / (20 * (pu + du)))
+      pre_first = pu + du > 0 ? (int)min((long long)p.mixed_grid, (6LL * p.mixed_grid * pu) / (5 * (pu + du)))
                               : p.mixed_grid;
     }
     s_pre_first = pre_first;
