@@ -1462,6 +1462,23 @@ struct DecPlanLds {
   int err, pps, n_full, n_items;
 };
 
+// Pages per decode split over `pages` pages of H kv-heads: about kDecItemsPerCU items per compute
+// unit, a multiple of 16, at least the host's bound, at least kDecLongSplitPages while that leaves
+// 2 items per compute unit, at most kMaxPagesPerSplit (the rule plan_kernel applies).
+__device__ __forceinline__ int dec_split_pages(unsigned long long pages, int H, int pps_min) {
+  long long pps = pps_min;
+  if (pages > 0) {
+    const long long units = (long long)pages * H;
+    const long long per = (long long)kPlanComputeUnits * kDecItemsPerCU;
+    const long long want = (units + per - 1) / per;
+    const long long two = (units + 2LL * kPlanComputeUnits - 1) / (2LL * kPlanComputeUnits);
+    pps = max(pps, (want + 15) / 16 * 16);
+    pps = max(pps, min((long long)kDecLongSplitPages, (two + 15) / 16 * 16));
+    pps = min(pps, (long long)max(pps_min, kMaxPagesPerSplit));
+  }
+  return (int)pps;
+}
+
 // Validates the lengths against the host bounds (any violation: no work, error 1) and builds the
 // list; splits beyond the workspace's partial slots give no work and error 2.  Ends with a barrier.
 // Sequences are taken kThreads at a time (chunks); a batch of at most kThreads sequences runs one.
@@ -1503,22 +1520,7 @@ __device__ __forceinline__ void decode_plan(const AttnArgs& a, const DecPlanArgs
     if (wave_bad) atomicOr(&P.err, 1);
   }
   __syncthreads();
-  if (tid == 0) {
-    // pages per split: about kDecItemsPerCU items per compute unit, a multiple of 16, at least the
-    // host's bound, at least kDecLongSplitPages while that leaves 2 items per compute unit, at
-    // most kMaxPagesPerSplit (the rule plan_kernel applies)
-    long long pps = d.pps_min;
-    if (P.pages > 0) {
-      const long long units = (long long)P.pages * H;
-      const long long per = (long long)kPlanComputeUnits * kDecItemsPerCU;
-      const long long want = (units + per - 1) / per;
-      const long long two = (units + 2LL * kPlanComputeUnits - 1) / (2LL * kPlanComputeUnits);
-      pps = max(pps, (want + 15) / 16 * 16);
-      pps = max(pps, min((long long)kDecLongSplitPages, (two + 15) / 16 * 16));
-      pps = min(pps, (long long)max(d.pps_min, kMaxPagesPerSplit));
-    }
-    P.pps = (int)pps;
-  }
+  if (tid == 0) P.pps = dec_split_pages(P.pages, H, d.pps_min);
   __syncthreads();
   const int pps = P.pps;
   const int err = P.err;
@@ -1615,6 +1617,68 @@ __device__ __forceinline__ void decode_plan(const AttnArgs& a, const DecPlanArgs
   __syncthreads();
 }
 
+// The same plan for batches of at most 64 sequences, built by wave 0 alone with a lane per
+// sequence: wave reductions, scans and ballots replace the LDS atomics and the barriers between
+// the phases (measured: the 8-wave plan spends about 3 us after the lengths arrive; most of it in
+// barriers).  The list is identical to decode_plan's.  Ends with a barrier.
+__device__ __forceinline__ void decode_plan_small(const AttnArgs& a, const DecPlanArgs& d, DecPlanLds& P) {
+  if (threadIdx.x < 64) {
+    const int lane = threadIdx.x, B = d.batch, H = a.num_kv_heads;
+    int pages = 0;
+    bool bad = false;
+    if (lane < B) {
+      const int ctx = d.ctx_lens[lane];
+      const long long kv = (long long)ctx + 1;
+      if (ctx < 0 || kv > d.max_kv_len || (kv + kPage - 1) / kPage > a.bt_stride) {
+        bad = true;
+      } else {
+        pages = (int)((kv + kPage - 1) / kPage);
+        P.kv[lane] = (int)kv;
+      }
+    }
+    const bool err = __any(bad);
+    unsigned total = pages;                         // 64 sequences of < 2^21 pages
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) total += __shfl_xor(total, off);
+    const int pps = dec_split_pages(total, H, d.pps_min);
+    if (err) pages = 0;
+    const int nf = pages / pps, rest = pages - nf * pps;
+    const int ns = nf + (rest > 0);
+    const int cls = rest > 0 ? part_bucket(rest, (float)kPartBuckets / (float)pps) : -1;
+    int incl_f = nf, incl_s = ns;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      const int vf = __shfl_up(incl_f, off), vs = __shfl_up(incl_s, off);
+      if (lane >= off) { incl_f += vf; incl_s += vs; }
+    }
+    const int tot_f = __shfl(incl_f, 63), tot_s = __shfl(incl_s, 63);
+    // position of a short split: the short splits of the classes before its own (class 0, the
+    // longest, first), then those of its class in sequence order
+    int pos = 0;
+    const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+    for (int k = 0; k < kPartBuckets; ++k) {
+      const unsigned long long m = __ballot(cls == k);
+      if (k < cls) pos += __popcll(m);
+      if (k == cls) pos += __popcll(m & below);
+    }
+    if (lane < B) {
+      P.full_pre[lane] = incl_f - nf;
+      P.split_pre[lane] = incl_s - ns;
+      if (cls >= 0) P.order[pos] = lane;
+    }
+    if (lane == 0) {
+      P.full_pre[B] = tot_f;
+      P.split_pre[B] = tot_s;
+      P.n_full = tot_f;
+      P.pps = pps;
+      P.err = err ? 1 : (tot_s > d.max_dec ? 2 : 0);
+      P.n_items = P.err ? 0 : tot_s * H;
+    }
+  }
+  __syncthreads();
+}
+
 // Work item `item` of the in-kernel plan: entries are the full splits in sequence order, then the
 // short last splits by size class; the kv-head runs fastest.
 __device__ __forceinline__ DecItem decode_item(const DecPlanLds& P, int item, int H, int B) {
@@ -1646,7 +1710,8 @@ __global__ __launch_bounds__(kThreads) void decode_kernel(AttnArgs a, DecPlanArg
   __shared__ int s_flag;
   int first = 0;
   if (threadIdx.x == 0) first = atomicAdd(&a.ws_hdr[kHdrCounter], 1);   // in flight during the plan
-  decode_plan(a, d, P);
+  if (d.batch <= 64) decode_plan_small(a, d, P);
+  else decode_plan(a, d, P);
   // the error flag shares a cache line with the work counter, so it is written only when set
   // (then no work follows); the prologue cleared it
   if (blockIdx.x == 0 && threadIdx.x == 0 && P.err) a.ws_hdr[kHdrError] = P.err;
