@@ -269,7 +269,7 @@ pearl_status set_error(pearl_status st, const char* fmt, ...) {
 int choose_pages_per_split(int batch, int num_kv_heads, int max_kv_len, int num_cu) {
   // The least pages per decode split, which sizes the workspace: about 16 decode items per
   // compute unit if every sequence were as long as the bound.  A split never holds fewer than 16
-  // pages (one page pair for each of the 8 waves), and its size is a multiple of 16 pages.  The
+  // pages (two pages for each of the 8 waves), and its size is a multiple of 16 pages.  The
   // planner takes larger splits from the launch's actual pages (kDecItemsPerCU).
   const int64_t max_pages = std::max<int64_t>(1, cdiv(std::max(max_kv_len, 1), kPage));
   const int64_t target = std::max<int64_t>(1, (int64_t)num_cu * 16);
