@@ -102,6 +102,25 @@ def test_random_small_decode(seed):
         assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="%s seed %d" % (mode, seed))
 
 
+@pytest.mark.parametrize("batch", [1, 63, 64, 65])
+def test_decode_planner_boundary(batch):
+    """Decode batches of at most 64 sequences are planned by one wave, larger ones by all 8 waves;
+    both lists must cover every split exactly once.  Contexts give several full splits per
+    sequence and short last splits of many sizes (and one sequence of a single key)."""
+    rng = np.random.default_rng(9100 + batch)
+    ctx = rng.integers(0, 2600, size=batch, endpoint=True)
+    ctx[0] = 0
+    if batch > 1:
+        ctx[1] = 16 * 64 - 1
+    say("case: decode planner boundary B=%d" % batch)
+    case = workloads.build_case("plan-bound", 9200 + batch, 8, 2, 128, ctx, np.ones(batch, np.int64), device="cuda")
+    kr, vr = _append_and_check(case)
+    o_ref, l_ref = oracle_full(case, kr, vr)
+    out, lse = gpu_attend(case, "decode")
+    torch.cuda.synchronize()
+    assert_close(bits(out), o_ref, lse.cpu().numpy(), l_ref, what="decode B=%d" % batch)
+
+
 def test_split_plans_agree():
     """The same decode with different split plans (a larger max_kv_len bound gives larger splits)
     agrees within tolerance; the same plan twice is bit-identical."""
