@@ -1147,22 +1147,25 @@ __device__ __forceinline__ int count_split_in(const AttnArgs& a, const DecItem& 
   return prev == it.n_splits - 1;
 }
 
-// One pipeline step: issue the next page's copies into s_next, then wait for the current page's
-// and consume it from s_cur.  The step is branch-free: a wave with no further page re-issues its
-// current page (cache hits, results unused), so every step leaves exactly one page in flight.
-// The copies are issued untracked, so the compiler adds no waits of its own for them (left to
-// itself it drained every copy in flight in one of the loop's two unrolled steps); s_next was last
-// read in the previous step, whose operand reads all completed before its MFMAs.
+// One pipeline step: issue the next page's copies into s_next (when the wave has one: `more`,
+// wave-uniform), then wait for the current page's and consume it from s_cur.  The copies are
+// issued untracked, so the compiler adds no waits of its own for them (left to itself it drained
+// every copy in flight in one of the loop's two unrolled steps); s_next was last read in the
+// previous step, whose operand reads all completed before its MFMAs.
 template <int D, bool kNew>
 __device__ __forceinline__ void decode_step(const AttnArgs& a, int p_cur, int p_nxt, int phys_nxt, int g, int kv,
                                             char* __restrict__ s_next, const char* __restrict__ s_cur,
                                             const bf16x8* qop, f32x4* oacc, float& m_run, float& l_run,
-                                            const NewRow& nr) {
+                                            const NewRow& nr, bool more) {
   constexpr int PAGE_LOADS = 2 * PageTile<D>::NDMA;   // vector-memory ops per page
-  decode_issue<D, kNew>(a, phys_nxt, p_nxt, g, kv, s_next, nr);
   // the current page has landed; the copies are invisible to the compiler, so the wait is also a
   // compiler barrier that keeps the stage reads below it
-  __asm__ volatile("s_waitcnt vmcnt(%0)" ::"n"(PAGE_LOADS) : "memory");
+  if (more) {
+    decode_issue<D, kNew>(a, phys_nxt, p_nxt, g, kv, s_next, nr);
+    __asm__ volatile("s_waitcnt vmcnt(%0)" ::"n"(PAGE_LOADS) : "memory");
+  } else {
+    __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  }
   decode_consume<D>(p_cur, kv, qop, oacc, m_run, l_run, a.scale_log2, s_cur);
 }
 
@@ -1224,24 +1227,26 @@ __device__ __forceinline__ void decode_split(const AttnArgs& a, const DecItem& i
   for (int mb = 0; mb < MB; ++mb) oacc[mb] = f32x4{0.f, 0.f, 0.f, 0.f};
   float m_run = -INFINITY, l_run = 0.f;
 
-  int nxt = min(w + NW, n_pg - 1);                 // past the last page: the current one again
+  // page indices past the wave's last page are clamped to the split's last page; such a page id is
+  // read but never copied
+  int nxt = min(w + NW, n_pg - 1);
   int ph_nxt = page_id(bt_row, p_begin + nxt, a.num_pages);
   for (int pi = w; pi < n_pg; pi += 2 * NW) {
     const int pj = pi + NW;
     const int n2 = min(pj + NW, n_pg - 1);
     const int ph_n2 = page_id(bt_row, p_begin + n2, a.num_pages);
     decode_step<D, kMergeHere>(a, p_begin + cur, p_begin + nxt, ph_nxt, g, kv, st1, st0, qop, oacc, m_run,
-                               l_run, nr);
+                               l_run, nr, pj < n_pg);
     if (pj >= n_pg) break;
     const int n3 = min(pj + 2 * NW, n_pg - 1);
     const int ph_n3 = page_id(bt_row, p_begin + n3, a.num_pages);
     decode_step<D, kMergeHere>(a, p_begin + nxt, p_begin + n2, ph_n2, g, kv, st0, st1, qop, oacc, m_run,
-                               l_run, nr);
+                               l_run, nr, pj + NW < n_pg);
     cur = n2;
     nxt = n3;
     ph_nxt = ph_n3;
   }
-  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");   // drain the trailing re-issued page
+  __asm__ volatile("s_waitcnt vmcnt(0)" ::: "memory");
   // the new row's bytes and page id are loaded now, to be stored once the LDS merge below has
   // waited for them
   const bool writer = kMergeHere && nr.page >= 0 && w == NW - 1 && lane < D / 8;
